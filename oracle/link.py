@@ -1,0 +1,131 @@
+"""Attention-level link step, written from Sec. 4.2 and Eq. (1) of the paper.
+
+Notation follows Sec. 4.2: the k' selected tokens are recomputed, K_exp / V_exp
+(N rows) hold the cached KV of the N - k' unselected tokens plus the
+recomputed rows "at correct positions", and A = softmax(Q K_exp^T . MASK) with
+MASK letting each selected token attend only to tokens at or before it.
+
+Readings where the paper is silent (each one is a choice, listed in the design doc):
+  * the logits are scaled by 1/sqrt(d) (standard attention; needed for
+    recompute-everything to equal an ordinary prefill);
+  * MASK is additive -inf (a masked key gets zero weight), and a token attends
+    to itself (key position <= query position);
+  * cached K keeps the rotary phase it was compiled with (no re-rotation);
+  * k larger than a chunk recomputes the whole chunk; k = 0 recomputes only the
+    suffix (the Naive scheme of Sec. 2.3); k < 0 means recompute every token
+    including the first chunk (FR, Sec. 2.3);
+  * GQA: query head h reads KV head floor(h / G), G = Hq / Hkv.
+"""
+from __future__ import annotations
+
+from typing import List, Sequence, Tuple
+
+import numpy as np
+
+
+def chunk_offsets(chunk_lens: Sequence[int]) -> List[int]:
+    """Linked position of each chunk's first token: the chunks are concatenated in order."""
+    offs, acc = [], 0
+    for length in chunk_lens:
+        offs.append(acc)
+        acc += int(length)
+    return offs
+
+
+def legolink_positions(chunk_lens: Sequence[int], suffix_len: int, k: int) -> np.ndarray:
+    """Linked positions of the selected set S (Sec. 4.2), ascending.
+
+    LegoLink-k selects the first k tokens of every chunk except the first, plus
+    every mutable (query) token, which sit after all chunks.  k < 0 selects all
+    tokens (FR).
+    """
+    offs = chunk_offsets(chunk_lens)
+    n_chunk_tokens = sum(int(x) for x in chunk_lens)
+    if k < 0:
+        return np.arange(n_chunk_tokens + suffix_len, dtype=np.int64)
+    sel = []
+    for j, (off, length) in enumerate(zip(offs, chunk_lens)):
+        if j == 0:
+            continue  # the first chunk is never recomputed
+        sel.extend(range(off, off + min(k, int(length))))
+    sel.extend(range(n_chunk_tokens, n_chunk_tokens + suffix_len))
+    return np.asarray(sel, dtype=np.int64)
+
+
+def expand_kv(cached_k: Sequence[np.ndarray], cached_v: Sequence[np.ndarray],
+              s_pos: np.ndarray, k_s: np.ndarray, v_s: np.ndarray,
+              n_total: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Build K_exp and V_exp [N, Hkv, d] (Sec. 4.2, third step).
+
+    cached_k[j], cached_v[j] are chunk j's cache [L_j, Hkv, d] exactly as the
+    compile step stored it.  Rows of S take the recomputed k_s / v_s; every
+    other row takes the cached vector of the chunk that holds that position.
+    """
+    hkv, d = k_s.shape[1], k_s.shape[2]
+    K = np.full((n_total, hkv, d), np.nan)
+    V = np.full((n_total, hkv, d), np.nan)
+    pos = 0
+    for ck, cv in zip(cached_k, cached_v):
+        K[pos:pos + ck.shape[0]] = ck
+        V[pos:pos + cv.shape[0]] = cv
+        pos += ck.shape[0]
+    K[s_pos] = k_s
+    V[s_pos] = v_s
+    if np.isnan(K).any() or np.isnan(V).any():
+        raise ValueError("a linked position has neither a cached nor a recomputed vector")
+    return K, V
+
+
+def masked_attention(q: np.ndarray, K_exp: np.ndarray, V_exp: np.ndarray, s_pos: np.ndarray,
+                     scale: float | None = None, rows: Sequence[int] | None = None,
+                     row_group: int = 256) -> Tuple[np.ndarray, np.ndarray]:
+    """Eq. (1): per selected row r at linked position p and head h,
+    A = softmax over keys i <= p of scale * <q[r,h], K_exp[i, h // G]>,
+    O = A . V_exp[:, h // G].  Returns out [n, Hq, d] and the natural-log
+    normaliser lse [n, Hq] (log of the softmax denominator, max included).
+
+    ``rows`` restricts the computation to some rows of S (each row is
+    independent); rows are processed ``row_group`` at a time to bound memory.
+    """
+    n_s, hq, d = q.shape
+    hkv = K_exp.shape[1]
+    G = hq // hkv
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    rows = np.arange(n_s) if rows is None else np.asarray(rows, dtype=np.int64)
+    out = np.zeros((len(rows), hq, d))
+    lse = np.zeros((len(rows), hq))
+    for g0 in range(0, len(rows), row_group):
+        rr = rows[g0:g0 + row_group]
+        p = s_pos[rr]
+        n_keys = int(p.max()) + 1
+        key_pos = np.arange(n_keys)
+        masked = key_pos[None, :] > p[:, None]          # key after the query: excluded
+        for h in range(hq):
+            g = h // G
+            logits = scale * (q[rr, h, :].astype(np.float64) @ K_exp[:n_keys, g, :].T)
+            logits[masked] = -np.inf
+            m = logits.max(axis=1, keepdims=True)
+            e = np.exp(logits - m)
+            denom = e.sum(axis=1, keepdims=True)
+            out[g0:g0 + len(rr), h, :] = (e @ V_exp[:n_keys, g, :]) / denom
+            lse[g0:g0 + len(rr), h] = (m + np.log(denom))[:, 0]
+    return out, lse
+
+
+def link_attention(chunk_lens: Sequence[int], suffix_len: int, k: int,
+                   cached_k: Sequence[np.ndarray], cached_v: Sequence[np.ndarray],
+                   q_s: np.ndarray, k_s: np.ndarray, v_s: np.ndarray,
+                   scale: float | None = None, rows: Sequence[int] | None = None):
+    """One attention layer of the link step for one request.
+
+    q_s, k_s, v_s are the recomputed rows of S in ascending position order
+    (already projected and rotated).  Returns (s_pos, out, lse, K_exp, V_exp).
+    """
+    s_pos = legolink_positions(chunk_lens, suffix_len, k)
+    if len(s_pos) != q_s.shape[0]:
+        raise ValueError(f"|S| = {len(s_pos)} but {q_s.shape[0]} query rows were given")
+    n_total = sum(int(x) for x in chunk_lens) + suffix_len
+    K_exp, V_exp = expand_kv(cached_k, cached_v, s_pos, k_s, v_s, n_total)
+    out, lse = masked_attention(q_s, K_exp, V_exp, s_pos, scale, rows)
+    return s_pos, out, lse, K_exp, V_exp

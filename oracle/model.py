@@ -1,0 +1,135 @@
+"""Model-level link step and compile step, for Llama-style decoders.
+
+Sec. 4.2 gives the per-layer recipe for the selected rows: project the k'
+hidden rows to Q, K, V, place K and V among the cached vectors of the other
+tokens, attend with the causal MASK, and apply W_O.  The rest of the layer is
+the model's own (Sec. 5.1 evaluates Llama / Mistral / Yi decoders), which the
+paper does not restate; this oracle uses the standard Llama layer: pre-norm
+RMSNorm, rotary embedding with the "rotate half" pairing (i, i + d/2) and
+inverse frequencies theta^(-2i/d), grouped-query attention, SwiGLU MLP, final
+RMSNorm.  No LM head (the link step ends at the last hidden state).
+
+The compile step (Sec. 2.2) runs one chunk alone through the same model with
+positions 0..L-1 and keeps each layer's K and V.
+
+Precision reading: weights, KV caches and the activations fed to a weight
+matrix are bf16; everything else is float64 here.  With ``bf16_storage`` the
+oracle rounds (round-to-nearest-even, via float32) exactly where a value is
+stored as bf16: the normalised activations entering a projection, q/k/v after
+the rotation, the attention output entering W_O and the SwiGLU product
+entering W_down.  The residual stream is never rounded.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Sequence, Tuple
+
+import numpy as np
+
+from .link import expand_kv, legolink_positions, masked_attention
+
+
+def _bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    u = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return u.view(np.float32).astype(np.float64)
+
+
+def _round_bf16(x: np.ndarray) -> np.ndarray:
+    """float64 -> float32 -> bf16 (nearest, ties to even) -> float64."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    u = (u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) & np.uint32(0xFFFF0000)
+    return u.view(np.float32).astype(np.float64)
+
+
+def rmsnorm(x: np.ndarray, w: np.ndarray, eps: float) -> np.ndarray:
+    """x / sqrt(mean(x^2) + eps) * w, row-wise."""
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * w
+
+
+def rope(x: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
+    """Rotate [n, H, d] by linked positions pos [n]; pairs (i, i + d/2), angle pos * theta^(-2i/d)."""
+    d = x.shape[-1]
+    half = d // 2
+    inv_freq = theta ** (-np.arange(half, dtype=np.float64) * 2.0 / d)
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]      # [n, d/2]
+    cos = np.cos(ang)[:, None, :]
+    sin = np.sin(ang)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
+
+
+def _silu(x: np.ndarray) -> np.ndarray:
+    return x / (1.0 + np.exp(-x))
+
+
+class _Cfg:
+    def __init__(self, hidden, ffn, hq, hkv, d, theta, eps):
+        self.hidden, self.ffn, self.hq, self.hkv, self.d = hidden, ffn, hq, hkv, d
+        self.theta, self.eps = theta, eps
+
+
+def _layer(h: np.ndarray, s_pos: np.ndarray, w: Dict[str, np.ndarray], cfg: _Cfg,
+           cached_k: Sequence[np.ndarray], cached_v: Sequence[np.ndarray], n_total: int,
+           bf16_storage: bool):
+    """One decoder layer for the selected rows h [nS, hidden] (float64, updated copy returned)."""
+    rnd = _round_bf16 if bf16_storage else (lambda a: a)
+    hq, hkv, d = cfg.hq, cfg.hkv, cfg.d
+    n = h.shape[0]
+    x = rnd(rmsnorm(h, _bf16_to_f64(w["attn_norm"]), cfg.eps))
+    qkv = x @ _bf16_to_f64(w["wqkv"]).T                                     # Q = E W_Q, K = E W_K, V = E W_V
+    q = qkv[:, : hq * d].reshape(n, hq, d)
+    k = qkv[:, hq * d: (hq + hkv) * d].reshape(n, hkv, d)
+    v = qkv[:, (hq + hkv) * d:].reshape(n, hkv, d)
+    q = rnd(rope(q, s_pos, cfg.theta))
+    k = rnd(rope(k, s_pos, cfg.theta))
+    v = rnd(v)
+    K_exp, V_exp = expand_kv(cached_k, cached_v, s_pos, k, v, n_total)    # recomputed rows at their positions
+    o, _ = masked_attention(q, K_exp, V_exp, s_pos)                          # Eq. (1)
+    o = rnd(o.reshape(n, hq * d))
+    h = h + o @ _bf16_to_f64(w["wo"]).T                                     # O = A V_exp W_O, residual
+    x2 = rnd(rmsnorm(h, _bf16_to_f64(w["mlp_norm"]), cfg.eps))
+    gu = x2 @ _bf16_to_f64(w["w_gate_up"]).T
+    a = rnd(_silu(gu[:, : cfg.ffn]) * gu[:, cfg.ffn:])
+    h = h + a @ _bf16_to_f64(w["w_down"]).T
+    return h, k, v
+
+
+def link_model(emb_s: np.ndarray, chunk_lens: Sequence[int], suffix_len: int, k: int,
+               weights: Sequence[Dict[str, np.ndarray]], final_norm: np.ndarray,
+               caches: Sequence[Tuple[Sequence[np.ndarray], Sequence[np.ndarray]]],
+               hidden: int, ffn: int, hq: int, hkv: int, d: int, theta: float, eps: float,
+               bf16_storage: bool = True):
+    """Full-model link step for one request.
+
+    emb_s [nS, hidden]: layer-0 hidden rows of S (embeddings of those tokens),
+    in ascending position order.  caches[l] = (chunk K list, chunk V list) of
+    layer l, each [L_j, Hkv, d] as compiled (float64 values of bf16 data).
+    Returns (s_pos, out [nS, hidden] after the final norm, per-layer recomputed
+    (k, v) of S).
+    """
+    cfg = _Cfg(hidden, ffn, hq, hkv, d, theta, eps)
+    s_pos = legolink_positions(chunk_lens, suffix_len, k)
+    if len(s_pos) != emb_s.shape[0]:
+        raise ValueError(f"|S| = {len(s_pos)} but {emb_s.shape[0]} embedding rows were given")
+    n_total = sum(int(x) for x in chunk_lens) + suffix_len
+    h = np.asarray(emb_s, dtype=np.float64)
+    new_kv = []
+    for layer, w in enumerate(weights):
+        ck, cv = caches[layer] if caches else ([], [])
+        h, ks, vs = _layer(h, s_pos, w, cfg, ck, cv, n_total, bf16_storage)
+        new_kv.append((ks, vs))
+    out = rmsnorm(h, _bf16_to_f64(final_norm), eps)
+    return s_pos, out, new_kv
+
+
+def compile_chunk(emb_chunk: np.ndarray, weights: Sequence[Dict[str, np.ndarray]],
+                  final_norm: np.ndarray, hidden: int, ffn: int, hq: int, hkv: int, d: int,
+                  theta: float, eps: float, bf16_storage: bool = True):
+    """Compile step (Sec. 2.2): prefill one chunk alone at positions 0..L-1.
+
+    This is the link step of a request with no cached chunks whose tokens are
+    all new, so every token is computed.  Returns (hidden out, per-layer (K, V)).
+    """
+    L = emb_chunk.shape[0]
+    _, out, kv = link_model(emb_chunk, [], L, 0, weights, final_norm, [([], [])] * len(weights),
+                            hidden, ffn, hq, hkv, d, theta, eps, bf16_storage)
+    return out, kv

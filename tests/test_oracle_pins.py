@@ -1,0 +1,346 @@
+"""Pins for the CPU oracle: each check ties it to something other than itself.
+
+* the worked selection examples in tests/golden (Sec. 4.2, by hand);
+* library causal attention (torch SDPA, float64) for recompute-everything (FR,
+  Sec. 2.3) and for the Naive scheme (k = 0, Sec. 2.3);
+* closed forms of softmax attention (constant V, zero query, a lone key,
+  one-hot V, one-hot K);
+* the HuggingFace Llama forward for the compile step (Sec. 2.2) and, through
+  prefix-caching / recompute-all identities, for the model-level link step.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import bf16_bits_to_f32, chunk_cache, final_norm_weight, model_weights, row_qkv
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "selection_examples.txt")
+
+
+def _read_golden():
+    cases = []
+    with open(GOLDEN) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            lens, suf, k, s = [x.strip() for x in line.split("|")]
+            cases.append(([int(x) for x in lens.split(",")], int(suf), int(k),
+                          [int(x) for x in s.split(",")] if s else []))
+    return cases
+
+
+@pytest.mark.parametrize("case", _read_golden())
+def test_selection_golden(case):
+    lens, suf, k, expect = case
+    assert oracle.legolink_positions(lens, suf, k).tolist() == expect
+
+
+def test_selection_size_closed_form():
+    rng = np.random.default_rng(1)
+    for _ in range(50):
+        lens = rng.integers(1, 40, size=rng.integers(1, 8)).tolist()
+        suf, k = int(rng.integers(0, 20)), int(rng.integers(0, 50))
+        s = oracle.legolink_positions(lens, suf, k)
+        assert len(s) == sum(min(k, L) for L in lens[1:]) + suf
+        assert np.all(np.diff(s) > 0)
+
+
+# ---------------------------------------------------------------- attention level
+
+def _f(x):
+    return bf16_bits_to_f32(x).astype(np.float64)
+
+
+def _case(lens, suf, k, hq, hkv, d, seed=5):
+    """Chunk caches and the recomputed rows of S for one request (float64 values of bf16 data)."""
+    ck, cv = [], []
+    for j, L in enumerate(lens):
+        a, b = chunk_cache(seed, j, L, hkv, d)
+        ck.append(_f(a)); cv.append(_f(b))
+    s_pos = oracle.legolink_positions(lens, suf, k)
+    q, kk, vv = row_qkv(seed, 0, s_pos, hq, hkv, d)
+    return ck, cv, _f(q), _f(kk), _f(vv)
+
+
+def _sdpa(q, K, V, mask):
+    """Library attention in float64: q [n, Hq, d], K/V [N, Hkv, d] (GQA by h // G), mask [n, N] bool."""
+    G = q.shape[1] // K.shape[1]
+    qt = torch.from_numpy(q).permute(1, 0, 2)[None]
+    Kt = torch.from_numpy(K).permute(1, 0, 2).repeat_interleave(G, dim=0)[None]
+    Vt = torch.from_numpy(V).permute(1, 0, 2).repeat_interleave(G, dim=0)[None]
+    o = torch.nn.functional.scaled_dot_product_attention(qt, Kt, Vt, attn_mask=torch.from_numpy(mask))
+    return o[0].permute(1, 0, 2).numpy()
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(4, 4, 16), (8, 2, 32)])
+def test_fr_equals_causal_prefill(hq, hkv, d):
+    """S = all tokens (FR): the link step is ordinary causal self-attention."""
+    lens, suf = [9, 13, 6], 5
+    ck, cv, q, k, v = _case(lens, suf, -1, hq, hkv, d)
+    s_pos, out, _, _, _ = oracle.link_attention(lens, suf, -1, ck, cv, q, k, v)
+    qt = torch.from_numpy(q).permute(1, 0, 2)[None]
+    G = hq // hkv
+    Kt = torch.from_numpy(k).permute(1, 0, 2).repeat_interleave(G, dim=0)[None]
+    Vt = torch.from_numpy(v).permute(1, 0, 2).repeat_interleave(G, dim=0)[None]
+    ref = torch.nn.functional.scaled_dot_product_attention(qt, Kt, Vt, is_causal=True)[0].permute(1, 0, 2)
+    np.testing.assert_allclose(out, ref.numpy(), rtol=0, atol=1e-12)
+
+
+def test_k0_equals_naive_concatenation():
+    """k = 0: only the suffix is computed; it attends to the caches concatenated as stored."""
+    lens, suf, hq, hkv, d = [7, 12, 5, 9], 6, 8, 4, 16
+    ck, cv, q, k, v = _case(lens, suf, 0, hq, hkv, d)
+    s_pos, out, _, _, _ = oracle.link_attention(lens, suf, 0, ck, cv, q, k, v)
+    K = np.concatenate(ck + [k], axis=0)
+    V = np.concatenate(cv + [v], axis=0)
+    n_c = sum(lens)
+    mask = np.arange(n_c + suf)[None, :] <= (n_c + np.arange(suf))[:, None]
+    np.testing.assert_allclose(out, _sdpa(q, K, V, mask), rtol=0, atol=1e-12)
+
+
+def test_placement_cached_equals_fresh():
+    """If every cached vector equals the recomputed one, LegoLink-k gives FR's rows of S.
+
+    Fails if a recomputed row, or a chunk's cache, is put at the wrong linked position.
+    """
+    lens, suf, hq, hkv, d, seed = [11, 17, 4, 20], 3, 4, 2, 16, 9
+    n = sum(lens) + suf
+    allq, allk, allv = (_f(a) for a in row_qkv(seed, 0, range(n), hq, hkv, d))
+    offs = oracle.chunk_offsets(lens)
+    ck = [allk[o:o + L] for o, L in zip(offs, lens)]
+    cv = [allv[o:o + L] for o, L in zip(offs, lens)]
+    mask = np.tril(np.ones((n, n), bool))
+    full = _sdpa(allq, allk, allv, mask)
+    for k in (0, 1, 3, 5, 100):
+        s = oracle.legolink_positions(lens, suf, k)
+        _, out, _, _, _ = oracle.link_attention(lens, suf, k, ck, cv, allq[s], allk[s], allv[s])
+        np.testing.assert_allclose(out, full[s], rtol=0, atol=1e-12)
+
+
+def test_one_hot_v_marks_recomputed_positions():
+    """V_exp = e_i for recomputed rows and 0 for cached rows: out's support is S up to the row."""
+    lens, suf, hq, hkv, k = [6, 5, 7], 4, 2, 1, 2
+    n = sum(lens) + suf
+    d = 32
+    ck, _, q, kk, _ = _case(lens, suf, k, hq, hkv, d)
+    cv = [np.zeros((L, hkv, d)) for L in lens]
+    s = oracle.legolink_positions(lens, suf, k)
+    vs = np.zeros((len(s), hkv, d))
+    vs[np.arange(len(s)), :, s] = 1.0
+    _, out, _, _, _ = oracle.link_attention(lens, suf, k, ck, cv, q, kk, vs)
+    for r, p in enumerate(s):
+        support = set(np.nonzero(out[r, 0] > 0)[0].tolist())
+        assert support == set(x for x in s.tolist() if x <= p)
+    # all-one-hot V (cached too): out is the attention row itself, masked entries exactly 0
+    cv = []
+    for o, L in zip(oracle.chunk_offsets(lens), lens):
+        z = np.zeros((L, hkv, d)); z[np.arange(L), :, o + np.arange(L)] = 1.0; cv.append(z)
+    _, out, _, _, _ = oracle.link_attention(lens, suf, k, ck, cv, q, kk, vs)
+    for r, p in enumerate(s):
+        assert np.all(out[r, :, p + 1: n] == 0.0)
+        np.testing.assert_allclose(out[r].sum(axis=-1), 1.0, atol=1e-13)
+
+
+def test_closed_forms():
+    lens, suf, hq, hkv, d, k = [5, 8], 4, 4, 2, 16, 3
+    ck, cv, q, kk, vv = _case(lens, suf, k, hq, hkv, d)
+    s = oracle.legolink_positions(lens, suf, k)
+    # constant V -> constant output
+    cvc = [np.full_like(x, 0.75) for x in cv]
+    _, out, _, _, _ = oracle.link_attention(lens, suf, k, ck, cvc, q, kk, np.full_like(vv, 0.75))
+    np.testing.assert_allclose(out, 0.75, atol=1e-14)
+    # zero query -> uniform weights: mean of V_exp[0..p], lse = log(p + 1)
+    _, out, lse, _, V = oracle.link_attention(lens, suf, k, ck, cv, np.zeros_like(q), kk, vv)
+    for r, p in enumerate(s):
+        for h in range(hq):
+            np.testing.assert_allclose(out[r, h], V[: p + 1, h // (hq // hkv)].mean(axis=0), atol=1e-13)
+        np.testing.assert_allclose(lse[r], np.log(p + 1), atol=1e-13)
+
+
+def test_position_zero_and_one_hot_keys():
+    """FR row at position 0 sees only itself; one-hot keys give a closed-form normaliser."""
+    lens, suf, hq, hkv, d = [4, 3], 2, 2, 2, 16
+    ck, cv, q, kk, vv = _case(lens, suf, -1, hq, hkv, d)
+    _, out, lse, _, _ = oracle.link_attention(lens, suf, -1, ck, cv, q, kk, vv)
+    np.testing.assert_allclose(out[0], vv[0], atol=1e-15)
+    np.testing.assert_allclose(lse[0], (q[0] * kk[0]).sum(-1) / np.sqrt(d), atol=1e-13)
+    # keys c * e_i, query e_j: row at p >= j has lse = log(p + exp(c / sqrt(d)))
+    n, c, j = sum(lens) + suf, 3.0, 2
+    kk1 = np.zeros_like(kk)
+    kk1[np.arange(n), :, np.arange(n)] = c
+    q1 = np.zeros_like(q)
+    q1[:, :, j] = 1.0
+    _, _, lse, _, _ = oracle.link_attention(lens, suf, -1, ck, cv, q1, kk1, vv)
+    for p in range(j, n):
+        np.testing.assert_allclose(lse[p], np.log(p + np.exp(c / np.sqrt(d))), atol=1e-13)
+
+
+def test_gqa_equals_replicated_mha():
+    lens, suf, k, d = [6, 9], 3, 2, 16
+    ck, cv, q, kk, vv = _case(lens, suf, k, 8, 2, d)
+    _, out_gqa, lse_gqa, _, _ = oracle.link_attention(lens, suf, k, ck, cv, q, kk, vv)
+    rep = lambda a: np.repeat(a, 4, axis=1)  # noqa: E731
+    _, out_mha, lse_mha, _, _ = oracle.link_attention(lens, suf, k, [rep(x) for x in ck],
+                                                      [rep(x) for x in cv], q, rep(kk), rep(vv))
+    np.testing.assert_allclose(out_gqa, out_mha, atol=1e-15)
+    np.testing.assert_allclose(lse_gqa, lse_mha, atol=1e-15)
+
+
+def test_lse_is_log_normaliser():
+    """exp(scale * q.k - lse) over allowed keys sums to 1 and reproduces out."""
+    lens, suf, k, hq, hkv, d = [10, 7, 12], 5, 4, 4, 2, 16
+    ck, cv, q, kk, vv = _case(lens, suf, k, hq, hkv, d)
+    s, out, lse, K, V = oracle.link_attention(lens, suf, k, ck, cv, q, kk, vv)
+    for r, p in enumerate(s):
+        for h in range(hq):
+            w = np.exp(K[: p + 1, h // 2] @ q[r, h] / np.sqrt(d) - lse[r, h])
+            np.testing.assert_allclose(w.sum(), 1.0, atol=1e-12)
+            np.testing.assert_allclose(w @ V[: p + 1, h // 2], out[r, h], atol=1e-12)
+
+
+# ---------------------------------------------------------------- model level
+
+TINY = dict(hidden=64, ffn=96, hq=4, hkv=2, d=16, theta=500000.0, eps=1e-5)
+
+
+def _tiny_weights(n_layers, seed=11):
+    ws = [model_weights(seed, l, TINY["hidden"], TINY["ffn"], TINY["hq"], TINY["hkv"], TINY["d"])
+          for l in range(n_layers)]
+    return ws, final_norm_weight(seed, TINY["hidden"])
+
+
+def _hf_model(ws, fn):
+    from transformers import LlamaConfig, LlamaModel
+
+    t = TINY
+    cfg = LlamaConfig(vocab_size=8, hidden_size=t["hidden"], intermediate_size=t["ffn"],
+                      num_hidden_layers=len(ws), num_attention_heads=t["hq"],
+                      num_key_value_heads=t["hkv"], head_dim=t["d"], rope_theta=t["theta"],
+                      rms_norm_eps=t["eps"], max_position_embeddings=4096,
+                      attention_bias=False, mlp_bias=False)
+    cfg._attn_implementation = "eager"
+    m = LlamaModel(cfg).double().eval()
+    f = lambda b: torch.from_numpy(_f(b))  # noqa: E731
+    qd, kd = t["hq"] * t["d"], t["hkv"] * t["d"]
+    with torch.no_grad():
+        for layer, w in zip(m.layers, ws):
+            wqkv = f(w["wqkv"])
+            layer.self_attn.q_proj.weight.copy_(wqkv[:qd])
+            layer.self_attn.k_proj.weight.copy_(wqkv[qd:qd + kd])
+            layer.self_attn.v_proj.weight.copy_(wqkv[qd + kd:])
+            layer.self_attn.o_proj.weight.copy_(f(w["wo"]))
+            gu = f(w["w_gate_up"])
+            layer.mlp.gate_proj.weight.copy_(gu[: t["ffn"]])
+            layer.mlp.up_proj.weight.copy_(gu[t["ffn"]:])
+            layer.mlp.down_proj.weight.copy_(f(w["w_down"]))
+            layer.input_layernorm.weight.copy_(f(w["attn_norm"]))
+            layer.post_attention_layernorm.weight.copy_(f(w["mlp_norm"]))
+        m.norm.weight.copy_(f(fn))
+    return m
+
+
+def test_compile_matches_hf_llama():
+    """Compile step = ordinary Llama prefill of one chunk at positions 0..L-1 (Sec. 2.2)."""
+    ws, fn = _tiny_weights(3)
+    L = 23
+    emb = np.random.default_rng(3).standard_normal((L, TINY["hidden"]))
+    out, kv = oracle.compile_chunk(emb, ws, fn, bf16_storage=False, **TINY)
+    m = _hf_model(ws, fn)
+    with torch.no_grad():
+        r = m(inputs_embeds=torch.from_numpy(emb)[None], position_ids=torch.arange(L)[None], use_cache=True)
+    # the HF RMSNorm computes in float32, hence the tolerance
+    np.testing.assert_allclose(out, r.last_hidden_state[0].numpy(), atol=2e-5, rtol=0)
+    for layer, (k, v) in enumerate(kv):
+        hk = r.past_key_values.layers[layer].keys[0].permute(1, 0, 2).numpy()
+        hv = r.past_key_values.layers[layer].values[0].permute(1, 0, 2).numpy()
+        np.testing.assert_allclose(k, hk, atol=2e-5, rtol=0)
+        np.testing.assert_allclose(v, hv, atol=2e-5, rtol=0)
+
+
+def _tok_emb(n_tokens, seed=4):
+    return np.random.default_rng(seed).standard_normal((n_tokens, TINY["hidden"]))
+
+
+def _compile_all(ws, fn, lens, emb, bf16):
+    caches_k = [[] for _ in ws]
+    caches_v = [[] for _ in ws]
+    for o, L in zip(oracle.chunk_offsets(lens), lens):
+        _, kv = oracle.compile_chunk(emb[o:o + L], ws, fn, bf16_storage=bf16, **TINY)
+        for layer, (k, v) in enumerate(kv):
+            caches_k[layer].append(k)
+            caches_v[layer].append(v)
+    return list(zip(caches_k, caches_v))
+
+
+@pytest.mark.parametrize("k", [0, 2, 7])
+def test_single_chunk_link_equals_prefill(k):
+    """One cached chunk + suffix: chunk 0 is never recomputed and its cache is exact
+    (it has no prefix), so the link step equals a full prefill of chunk + suffix."""
+    ws, fn = _tiny_weights(2)
+    lens, suf = [19], 6
+    emb = _tok_emb(sum(lens) + suf)
+    caches = _compile_all(ws, fn, lens, emb, bf16=False)
+    s, out, _ = oracle.link_model(emb[19:], lens, suf, k, ws, fn, caches, bf16_storage=False, **TINY)
+    full, _ = oracle.compile_chunk(emb, ws, fn, bf16_storage=False, **TINY)
+    np.testing.assert_allclose(out, full[s], atol=1e-10, rtol=0)
+
+
+def test_recompute_whole_chunks_equals_prefill():
+    """k >= every chunk length recomputes all chunks but the first, whose cache is exact:
+    the link step equals the full prefill (FR) on every selected row."""
+    ws, fn = _tiny_weights(2)
+    lens, suf = [9, 6, 11], 4
+    emb = _tok_emb(sum(lens) + suf, seed=8)
+    caches = _compile_all(ws, fn, lens, emb, bf16=False)
+    s = oracle.legolink_positions(lens, suf, 11)
+    _, out, kv = oracle.link_model(emb[s], lens, suf, 11, ws, fn, caches, bf16_storage=False, **TINY)
+    full, fkv = oracle.compile_chunk(emb, ws, fn, bf16_storage=False, **TINY)
+    np.testing.assert_allclose(out, full[s], atol=1e-10, rtol=0)
+    for (k1, v1), (k2, v2) in zip(kv, fkv):
+        np.testing.assert_allclose(k1, k2[s], atol=1e-10, rtol=0)
+        np.testing.assert_allclose(v1, v2[s], atol=1e-10, rtol=0)
+
+
+def test_link_differs_from_prefill_when_caches_are_position_independent():
+    """With several chunks and small k the link step is an approximation: the cached
+    rows of later chunks were compiled at positions from 0, so the result differs
+    from FR (guards against an oracle that silently recomputes everything)."""
+    ws, fn = _tiny_weights(2)
+    lens, suf = [9, 6, 11], 4
+    emb = _tok_emb(sum(lens) + suf, seed=8)
+    caches = _compile_all(ws, fn, lens, emb, bf16=False)
+    s = oracle.legolink_positions(lens, suf, 1)
+    _, out, _ = oracle.link_model(emb[s], lens, suf, 1, ws, fn, caches, bf16_storage=False, **TINY)
+    full, _ = oracle.compile_chunk(emb, ws, fn, bf16_storage=False, **TINY)
+    assert np.abs(out - full[s]).max() > 1e-3
+
+
+def test_bf16_storage_stays_close():
+    """Rounding at the bf16 storage points moves the result by about bf16 precision only."""
+    ws, fn = _tiny_weights(2)
+    lens, suf, k = [9, 6, 11], 4, 3
+    emb = _tok_emb(sum(lens) + suf, seed=8)
+    s = oracle.legolink_positions(lens, suf, k)
+    c64 = _compile_all(ws, fn, lens, emb, bf16=False)
+    c16 = _compile_all(ws, fn, lens, emb, bf16=True)
+    _, o64, _ = oracle.link_model(emb[s], lens, suf, k, ws, fn, c64, bf16_storage=False, **TINY)
+    _, o16, _ = oracle.link_model(emb[s], lens, suf, k, ws, fn, c16, bf16_storage=True, **TINY)
+    assert np.abs(o64 - o16).max() < 5e-2
+
+
+def test_rope_properties():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((5, 3, 16))
+    pos = np.array([0, 1, 7, 1000, 131071])
+    y = oracle.rope(x, pos, 500000.0)
+    np.testing.assert_allclose(y[0], x[0], atol=0)                     # position 0: identity
+    np.testing.assert_allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-13)
+    # relative position: <R(a) q, R(b) k> depends on a - b only
+    q, k = rng.standard_normal((1, 1, 16)), rng.standard_normal((1, 1, 16))
+    d1 = (oracle.rope(q, np.array([50]), 1e4) * oracle.rope(k, np.array([20]), 1e4)).sum()
+    d2 = (oracle.rope(q, np.array([130]), 1e4) * oracle.rope(k, np.array([100]), 1e4)).sum()
+    np.testing.assert_allclose(d1, d2, rtol=1e-12)
