@@ -1,0 +1,376 @@
+// Host planner of the link step: integer work only, no device calls.
+//
+// Builds, for a batch of requests, the selected set S (LegoLink-k, Sec. 4.2:
+// the first k tokens of every chunk but the first, plus the suffix; k < 0 =
+// every token, Sec. 2.3), the linked block tables (chunks concatenated in
+// order, then the suffix), the request-private blocks that receive recomputed
+// K/V (copy-on-write when a block also keeps cached rows), and the attention
+// work decomposition (query tiles x split-KV key ranges).
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+#include "plan_internal.h"
+#include "status.h"
+
+namespace epic {
+
+epic_status validate_attn_cfg(const epic_attn_cfg* cfg) {
+  EPIC_CHECK_ARG(cfg != nullptr, "attention config is NULL");
+  if (cfg->num_kv_heads <= 0 || cfg->num_q_heads <= 0 || cfg->num_q_heads % cfg->num_kv_heads != 0)
+    return fail(EPIC_ERR_INVALID_ARG, "num_q_heads (%d) must be a positive multiple of num_kv_heads (%d)",
+                cfg->num_q_heads, cfg->num_kv_heads);
+  const int G = cfg->num_q_heads / cfg->num_kv_heads;
+  if ((G & (G - 1)) != 0 || G > kTileRows)
+    return fail(EPIC_ERR_UNSUPPORTED, "query heads per KV head (%d) must be a power of two <= %d", G, kTileRows);
+  if (cfg->head_dim != 64 && cfg->head_dim != 128)
+    return fail(EPIC_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", cfg->head_dim);
+  if (cfg->block_size != kBlock)
+    return fail(EPIC_ERR_UNSUPPORTED, "block_size %d not supported (16)", cfg->block_size);
+  if (cfg->kv_split_blocks < 0)
+    return fail(EPIC_ERR_INVALID_ARG, "kv_split_blocks %d < 0", cfg->kv_split_blocks);
+  if (!(cfg->softmax_scale >= 0.0f)) return fail(EPIC_ERR_INVALID_ARG, "softmax_scale must be >= 0");
+  return EPIC_OK;
+}
+
+namespace {
+
+int cdiv(int64_t a, int64_t b) { return static_cast<int>((a + b - 1) / b); }
+
+struct ReqShape {
+  int64_t n_chunk_tokens = 0;
+  int n_s = 0, n_lb = 0, n_priv = 0;
+};
+
+// Number of tokens of chunk j that belong to S.
+int selected_in_chunk(const epic_link_request& r, int j) {
+  if (r.k < 0) return r.chunk_len[j];
+  if (j == 0) return 0;  // the first chunk is never recomputed
+  return std::min(r.k, r.chunk_len[j]);
+}
+
+epic_status validate_request(const epic_link_request& r, int idx, ReqShape* sh) {
+  EPIC_CHECK_ARG(r.num_chunks >= 0, "request %d: num_chunks %d < 0", idx, r.num_chunks);
+  EPIC_CHECK_ARG(r.suffix_len >= 0, "request %d: suffix_len %d < 0", idx, r.suffix_len);
+  if (r.num_chunks > 0) {
+    EPIC_CHECK_ARG(r.chunk_len && r.chunk_block_off && r.chunk_blocks,
+                   "request %d: chunk arrays are NULL", idx);
+    EPIC_CHECK_ARG(r.chunk_block_off[0] == 0, "request %d: chunk_block_off[0] != 0", idx);
+  }
+  *sh = ReqShape{};
+  for (int j = 0; j < r.num_chunks; ++j) {
+    const int L = r.chunk_len[j];
+    EPIC_CHECK_ARG(L >= 1, "request %d chunk %d: length %d < 1", idx, j, L);
+    const int nb = r.chunk_block_off[j + 1] - r.chunk_block_off[j];
+    EPIC_CHECK_ARG(nb == cdiv(L, kBlock), "request %d chunk %d: %d blocks given, %d needed", idx, j, nb,
+                   cdiv(L, kBlock));
+    sh->n_chunk_tokens += L;
+    const int sel = selected_in_chunk(r, j);
+    sh->n_s += sel;
+    sh->n_lb += nb;
+    sh->n_priv += cdiv(sel, kBlock);
+  }
+  sh->n_s += r.suffix_len;
+  sh->n_lb += cdiv(r.suffix_len, kBlock);
+  sh->n_priv += cdiv(r.suffix_len, kBlock);
+  EPIC_CHECK_ARG(sh->n_chunk_tokens + r.suffix_len < (int64_t(1) << 30), "request %d: too many tokens", idx);
+  return EPIC_OK;
+}
+
+// Linked positions of S for one request, ascending.
+void select_positions(const epic_link_request& r, std::vector<int32_t>* pos) {
+  int64_t off = 0;
+  for (int j = 0; j < r.num_chunks; ++j) {
+    const int sel = selected_in_chunk(r, j);
+    for (int t = 0; t < sel; ++t) pos->push_back(static_cast<int32_t>(off + t));
+    off += r.chunk_len[j];
+  }
+  for (int t = 0; t < r.suffix_len; ++t) pos->push_back(static_cast<int32_t>(off + t));
+}
+
+// Linked block table of one request: (pos0, len) of each block in position order.
+void linked_blocks(const epic_link_request& r, std::vector<int32_t>* pos0, std::vector<int32_t>* len) {
+  int64_t off = 0;
+  for (int j = 0; j < r.num_chunks; ++j) {
+    for (int t = 0; t < r.chunk_len[j]; t += kBlock) {
+      pos0->push_back(static_cast<int32_t>(off + t));
+      len->push_back(std::min(kBlock, r.chunk_len[j] - t));
+    }
+    off += r.chunk_len[j];
+  }
+  for (int t = 0; t < r.suffix_len; t += kBlock) {
+    pos0->push_back(static_cast<int32_t>(off + t));
+    len->push_back(std::min(kBlock, r.suffix_len - t));
+  }
+}
+
+struct Tile {
+  int req, row0, nrows, nblk;
+};
+
+// Query tiles: consecutive S rows of one request, rows_per_tile at a time.  A
+// tile needs the linked blocks whose first position is <= its last row's position.
+void make_tiles(const epic_link_request* reqs, int batch, int rows_per_tile, std::vector<Tile>* tiles,
+                int64_t* total_blocks) {
+  *total_blocks = 0;
+  int row_base = 0;
+  for (int b = 0; b < batch; ++b) {
+    std::vector<int32_t> pos, p0, ln;
+    select_positions(reqs[b], &pos);
+    linked_blocks(reqs[b], &p0, &ln);
+    for (size_t r0 = 0; r0 < pos.size(); r0 += rows_per_tile) {
+      const int n = static_cast<int>(std::min<size_t>(rows_per_tile, pos.size() - r0));
+      const int32_t last = pos[r0 + n - 1];
+      const int nblk = static_cast<int>(std::upper_bound(p0.begin(), p0.end(), last) - p0.begin());
+      tiles->push_back(Tile{b, row_base + static_cast<int>(r0), n, nblk});
+      *total_blocks += nblk;
+    }
+    row_base += static_cast<int>(pos.size());
+  }
+}
+
+// Key blocks per split-KV work item.  Rows are split only as far as needed to
+// give about kTargetItems workgroups (8 per CU of 256 CUs, two resident at a
+// time), halving from "no split"; a split never goes below 32 blocks (512
+// keys).  Fewer splits mean fewer partial results to write and merge.
+int split_blocks(const epic_attn_cfg* cfg, const std::vector<Tile>& tiles) {
+  if (cfg->kv_split_blocks > 0) return std::max(kKvTileBlocks, cfg->kv_split_blocks / kKvTileBlocks * kKvTileBlocks);
+  constexpr int64_t kTargetItems = 2048;
+  int max_nblk = kKvTileBlocks;
+  for (const Tile& t : tiles) max_nblk = std::max(max_nblk, t.nblk);
+  int split = (max_nblk + kKvTileBlocks - 1) / kKvTileBlocks * kKvTileBlocks;
+  while (split > 32) {
+    int64_t items = 0;
+    for (const Tile& t : tiles) items += std::max(1, cdiv(t.nblk, split));
+    if (items * cfg->num_kv_heads >= kTargetItems) break;
+    split = std::max(32, (split / 2 + kKvTileBlocks - 1) / kKvTileBlocks * kKvTileBlocks);
+  }
+  return split;
+}
+
+int64_t align16(int64_t n) { return (n + 15) & ~int64_t(15); }
+
+}  // namespace
+
+}  // namespace epic
+
+using namespace epic;
+
+extern "C" epic_status epic_plan_sizes_get(const epic_link_request* reqs, int32_t batch,
+                                           const epic_attn_cfg* cfg, int32_t n_free,
+                                           epic_plan_sizes* out) {
+  clear_error();
+  EPIC_CHECK_ARG(out != nullptr, "output sizes pointer is NULL");
+  EPIC_CHECK_ARG(batch >= 0, "batch %d < 0", batch);
+  EPIC_CHECK_ARG(batch == 0 || reqs != nullptr, "requests pointer is NULL");
+  EPIC_CHECK_ARG(n_free >= 0, "n_free %d < 0", n_free);
+  epic_status st = validate_attn_cfg(cfg);
+  if (st != EPIC_OK) return st;
+  epic_plan_sizes s{};
+  s.batch = batch;
+  s.tile_rows = kTileRows;
+  int64_t n_s = 0, n_lb = 0, n_priv = 0, max_pos = 0;
+  for (int b = 0; b < batch; ++b) {
+    ReqShape sh;
+    st = validate_request(reqs[b], b, &sh);
+    if (st != EPIC_OK) return st;
+    n_s += sh.n_s;
+    n_lb += sh.n_lb;
+    n_priv += sh.n_priv;
+    max_pos = std::max<int64_t>(max_pos, sh.n_chunk_tokens + reqs[b].suffix_len);
+  }
+  EPIC_CHECK_ARG(n_s < (int64_t(1) << 30) && n_lb < (int64_t(1) << 30), "batch too large");
+  if (n_priv > n_free)
+    return fail(EPIC_ERR_NO_PRIVATE_BLOCKS, "plan needs %lld private blocks, %d free", (long long)n_priv, n_free);
+  const int G = cfg->num_q_heads / cfg->num_kv_heads;
+  std::vector<Tile> tiles;
+  int64_t total_blocks = 0;
+  make_tiles(reqs, batch, kTileRows / G, &tiles, &total_blocks);
+  const int split = split_blocks(cfg, tiles);
+  int64_t n_work = 0, n_part = 0;
+  for (const Tile& t : tiles) {
+    const int ns = std::max(1, cdiv(t.nblk, split));
+    n_work += ns;
+    if (ns > 1) n_part += ns;
+  }
+  s.n_s = static_cast<int32_t>(n_s);
+  s.n_linked_blocks = static_cast<int32_t>(n_lb);
+  s.n_private = static_cast<int32_t>(n_priv);
+  s.n_tiles = static_cast<int32_t>(tiles.size());
+  s.n_work = static_cast<int32_t>(n_work);
+  s.n_partials = static_cast<int32_t>(n_part);
+  s.max_pos = static_cast<int32_t>(max_pos);
+  s.total_ints = 3 * align16(n_s) + 2 * align16(batch + 1) + 3 * align16(n_lb) + 2 * align16(n_priv) +
+                 align16(n_priv * kBlock) + align16(4 * int64_t(tiles.size())) + align16(4 * n_work);
+  *out = s;
+  return EPIC_OK;
+}
+
+extern "C" epic_status epic_plan_layout(const epic_plan_sizes* s, int32_t* base, epic_plan* p) {
+  clear_error();
+  EPIC_CHECK_ARG(s && p, "NULL argument");
+  int32_t* cur = base;
+  auto take = [&](int64_t n) {
+    int32_t* r = cur;
+    cur += align16(n);
+    return r;
+  };
+  p->s_pos = take(s->n_s);
+  p->s_req = take(s->n_s);
+  p->s_slot = take(s->n_s);
+  p->s_off = take(s->batch + 1);
+  p->linked_blocks = take(s->n_linked_blocks);
+  p->block_pos0 = take(s->n_linked_blocks);
+  p->block_len = take(s->n_linked_blocks);
+  p->blk_off = take(s->batch + 1);
+  p->priv_block = take(s->n_private);
+  p->priv_src = take(s->n_private);
+  p->priv_rows = take(int64_t(s->n_private) * kBlock);
+  p->tiles = take(4 * int64_t(s->n_tiles));
+  p->work = take(4 * int64_t(s->n_work));
+  if (cur - base != s->total_ints) return fail(EPIC_ERR_INVALID_ARG, "plan sizes are inconsistent");
+  return EPIC_OK;
+}
+
+extern "C" epic_status epic_plan_link(const epic_link_request* reqs, int32_t batch,
+                                      const epic_attn_cfg* cfg, const int32_t* free_blocks,
+                                      int32_t n_free, int32_t num_blocks,
+                                      const epic_plan_sizes* sizes, epic_plan* plan) {
+  epic_plan_sizes chk;
+  epic_status st = epic_plan_sizes_get(reqs, batch, cfg, n_free, &chk);
+  if (st != EPIC_OK) return st;
+  EPIC_CHECK_ARG(sizes && plan, "NULL sizes or plan");
+  EPIC_CHECK_ARG(std::memcmp(&chk, sizes, sizeof(chk)) == 0, "sizes do not match these requests");
+  EPIC_CHECK_ARG(num_blocks > 0, "num_blocks %d <= 0", num_blocks);
+  EPIC_CHECK_ARG(chk.n_private == 0 || free_blocks != nullptr, "free_blocks is NULL");
+
+  // Block ids: chunk blocks and free blocks in range, free blocks distinct and unused by chunks.
+  std::vector<uint8_t> used(static_cast<size_t>(num_blocks), 0);
+  for (int b = 0; b < batch; ++b) {
+    const epic_link_request& r = reqs[b];
+    const int nb = r.num_chunks > 0 ? r.chunk_block_off[r.num_chunks] : 0;
+    for (int i = 0; i < nb; ++i) {
+      const int id = r.chunk_blocks[i];
+      EPIC_CHECK_ARG(id >= 0 && id < num_blocks, "request %d: chunk block id %d out of range [0, %d)", b, id,
+                     num_blocks);
+      used[id] = 1;
+    }
+  }
+  for (int i = 0; i < chk.n_private; ++i) {
+    const int id = free_blocks[i];
+    EPIC_CHECK_ARG(id >= 0 && id < num_blocks, "free block id %d out of range [0, %d)", id, num_blocks);
+    EPIC_CHECK_ARG(used[id] == 0, "free block %d is a chunk block or listed twice", id);
+    used[id] = 2;
+  }
+
+  const int bs = kBlock;
+  int row = 0, lb = 0, pv = 0;
+  for (int b = 0; b < batch; ++b) {
+    const epic_link_request& r = reqs[b];
+    plan->s_off[b] = row;
+    plan->blk_off[b] = lb;
+    int64_t off = 0;
+    // chunk tokens
+    for (int j = 0; j < r.num_chunks; ++j) {
+      const int L = r.chunk_len[j];
+      const int sel = selected_in_chunk(r, j);  // tokens [0, sel) of the chunk are in S
+      const int32_t* cb = r.chunk_blocks + r.chunk_block_off[j];
+      for (int i = 0; i * bs < L; ++i) {
+        const int t0 = i * bs, len = std::min(bs, L - t0);
+        plan->block_pos0[lb] = static_cast<int32_t>(off + t0);
+        plan->block_len[lb] = len;
+        if (t0 < sel) {
+          const int id = free_blocks[pv];
+          const bool keeps_cached = sel < t0 + len;  // some valid slot is not recomputed
+          plan->priv_block[pv] = id;
+          plan->priv_src[pv] = keeps_cached ? cb[i] : -1;
+          for (int o = 0; o < bs; ++o) {
+            const int t = t0 + o;
+            int32_t rr = -1;
+            if (t < sel) {
+              rr = row++;
+              plan->s_pos[rr] = static_cast<int32_t>(off + t);
+              plan->s_req[rr] = b;
+              plan->s_slot[rr] = id * bs + o;
+            }
+            plan->priv_rows[int64_t(pv) * bs + o] = rr;
+          }
+          plan->linked_blocks[lb] = id;
+          ++pv;
+        } else {
+          plan->linked_blocks[lb] = cb[i];
+        }
+        ++lb;
+      }
+      off += L;
+    }
+    // suffix tokens: all new, all in S
+    for (int t0 = 0; t0 < r.suffix_len; t0 += bs) {
+      const int len = std::min(bs, r.suffix_len - t0);
+      const int id = free_blocks[pv];
+      plan->block_pos0[lb] = static_cast<int32_t>(off + t0);
+      plan->block_len[lb] = len;
+      plan->linked_blocks[lb] = id;
+      plan->priv_block[pv] = id;
+      plan->priv_src[pv] = -1;
+      for (int o = 0; o < bs; ++o) {
+        int32_t rr = -1;
+        if (o < len) {
+          rr = row++;
+          plan->s_pos[rr] = static_cast<int32_t>(off + t0 + o);
+          plan->s_req[rr] = b;
+          plan->s_slot[rr] = id * bs + o;
+        }
+        plan->priv_rows[int64_t(pv) * bs + o] = rr;
+      }
+      ++pv;
+      ++lb;
+    }
+  }
+  plan->s_off[batch] = row;
+  plan->blk_off[batch] = lb;
+  if (row != chk.n_s || lb != chk.n_linked_blocks || pv != chk.n_private)
+    return fail(EPIC_ERR_INVALID_ARG, "internal planner inconsistency");
+
+  // Attention tiles and split-KV work items.  Work items are ordered key
+  // segment first, so that the workgroups running at the same time read the
+  // same KV blocks (one L2 per XCD serves them).
+  const int G = cfg->num_q_heads / cfg->num_kv_heads;
+  std::vector<Tile> tiles;
+  int64_t total_blocks = 0;
+  make_tiles(reqs, batch, kTileRows / G, &tiles, &total_blocks);
+  const int split = split_blocks(cfg, tiles);
+  int part = 0, max_splits = 1;
+  for (size_t t = 0; t < tiles.size(); ++t) {
+    const int ns = std::max(1, cdiv(tiles[t].nblk, split));
+    max_splits = std::max(max_splits, ns);
+    plan->tiles[4 * t + 0] = tiles[t].row0;
+    plan->tiles[4 * t + 1] = tiles[t].nrows;
+    plan->tiles[4 * t + 2] = ns > 1 ? part : -1;
+    plan->tiles[4 * t + 3] = ns;
+    if (ns > 1) part += ns;
+  }
+  // inside a segment, tiles with the longest key range go first (the tail of
+  // the launch then holds the short items)
+  std::vector<int> order(tiles.size());
+  for (size_t t = 0; t < tiles.size(); ++t) order[t] = static_cast<int>(t);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return tiles[x].nblk > tiles[y].nblk; });
+  int w = 0;
+  for (int seg = 0; seg < max_splits; ++seg) {
+    for (int t : order) {
+      const int ns = plan->tiles[4 * t + 3];
+      if (seg >= ns) continue;
+      const int base = plan->blk_off[tiles[t].req];
+      const int b0 = base + seg * split;
+      const int b1 = base + std::min(tiles[t].nblk, (seg + 1) * split);
+      plan->work[4 * w + 0] = static_cast<int32_t>(t);
+      plan->work[4 * w + 1] = b0;
+      plan->work[4 * w + 2] = b1;
+      plan->work[4 * w + 3] = ns > 1 ? plan->tiles[4 * t + 2] + seg : -1;
+      ++w;
+    }
+  }
+  if (w != chk.n_work || part != chk.n_partials)
+    return fail(EPIC_ERR_INVALID_ARG, "internal planner inconsistency (work)");
+  return EPIC_OK;
+}

@@ -1,0 +1,45 @@
+"""The C-ABI library loads without a GPU and exports every entry point the header declares."""
+import ctypes
+import os
+import re
+
+from paper_2410_15332_amd import epic_link as el
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = []
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names += re.findall(r"^[A-Za-z_][\w\s\*]*?\b(epic_\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_entry_points():
+    d = _declared()
+    for name in ("epic_plan_link", "epic_link_attention", "epic_link_layer", "epic_link_model"):
+        assert name in d
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(el._LIB_PATH)
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert sorted(el.EXPORTED) == _declared()
+
+
+def test_status_strings_and_version():
+    assert el.epic_status_string(0) == "ok"
+    assert "workspace" in el.epic_status_string(4)
+    assert "gfx950" in el.epic_version()
+
+
+def test_workspace_bytes_scale_with_partials():
+    cfg = el.attn_cfg(32, 8, 128, 0.0, 8)
+    reqs = [el.Request([512] * 4, [list(range(32 * j, 32 * j + 32)) for j in range(4)], 64, 16)]
+    s = el.epic_plan_sizes_get(reqs, cfg, 1000)
+    assert s.n_partials > 0
+    assert el.epic_link_workspace_bytes(cfg, s) >= s.n_partials * 8 * 128 * (128 + 1) * 4

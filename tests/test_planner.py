@@ -1,0 +1,175 @@
+"""Host planner (integer, CPU only): bit-exact against the oracle's selection and
+the definitions of the linked block table, copy-on-write blocks and work items."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2410_15332_amd import epic_link as el
+
+
+def _random_requests(rng, batch, max_chunks=6, max_len=70, pool=None):
+    reqs, nxt = [], 0
+    for _ in range(batch):
+        m = int(rng.integers(0, max_chunks + 1))
+        lens = [int(x) for x in rng.integers(1, max_len, size=m)]
+        blocks = []
+        for L in lens:
+            nb = -(-L // 16)
+            blocks.append(list(range(nxt, nxt + nb)))
+            nxt += nb
+        k = int(rng.choice([-1, 0, 1, 3, 16, 17, 40, 100]))
+        reqs.append(el.Request(lens, blocks, int(rng.integers(0, 40)), k))
+    return reqs, nxt
+
+
+def _plan(reqs, n_used, hq=8, hkv=2, d=128, split=0, extra=3):
+    cfg = el.attn_cfg(hq, hkv, d, 0.0, split)
+    need = el.epic_plan_sizes_get(reqs, cfg, 1 << 30).n_private
+    free = list(range(n_used, n_used + need + extra))
+    sizes, buf, v = el.epic_plan_link(reqs, cfg, free, n_used + need + extra)
+    return cfg, sizes, v, free
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("hq,hkv", [(8, 8), (32, 8), (16, 2)])
+def test_plan_matches_definitions(seed, hq, hkv):
+    rng = np.random.default_rng(seed)
+    reqs, n_used = _random_requests(rng, int(rng.integers(1, 5)))
+    cfg, sizes, v, free = _plan(reqs, n_used, hq, hkv, split=int(rng.choice([0, 4, 8, 12])))
+    assert sizes.batch == len(reqs)
+    priv_seen = []
+    for r, req in enumerate(reqs):
+        s = oracle.legolink_positions(req.chunk_lens, req.suffix_len, req.k)
+        a, b = v["s_off"][r], v["s_off"][r + 1]
+        assert v["s_pos"][a:b].tolist() == s.tolist()
+        assert np.all(v["s_req"][a:b] == r)
+        # linked block table: contiguous positions, chunk blocks in order, suffix last
+        b0, b1 = v["blk_off"][r], v["blk_off"][r + 1]
+        pos0, blen, phys = v["block_pos0"][b0:b1], v["block_len"][b0:b1], v["linked_blocks"][b0:b1]
+        assert pos0[0] == 0 if b1 > b0 else True
+        assert np.all(pos0[1:] == pos0[:-1] + blen[:-1])
+        n_total = sum(req.chunk_lens) + req.suffix_len
+        assert (pos0[-1] + blen[-1] if b1 > b0 else 0) == n_total
+        s_set = set(s.tolist())
+        lb = 0
+        off = 0
+        shared = {}
+        for L, blocks in zip(req.chunk_lens, req.chunk_blocks):
+            for i, bid in enumerate(blocks):
+                shared[b0 + lb] = bid
+                lb += 1
+            off += L
+        for i in range(b1 - b0):
+            toks = set(range(pos0[i], pos0[i] + blen[i]))
+            if toks & s_set:
+                assert phys[i] in free
+                priv_seen.append(int(phys[i]))
+            else:
+                assert phys[i] == shared[b0 + i]
+    # private blocks: taken in order, each once; COW iff the block keeps cached rows
+    assert v["priv_block"].tolist() == free[:sizes.n_private]
+    assert sorted(priv_seen) == sorted(v["priv_block"].tolist())
+    rows = v["priv_rows"].reshape(-1, 16)
+    for p in range(sizes.n_private):
+        for o in range(16):
+            rr = rows[p, o]
+            if rr >= 0:
+                assert v["s_slot"][rr] == v["priv_block"][p] * 16 + o
+    covered = sorted(int(x) for x in rows.ravel() if x >= 0)
+    assert covered == list(range(sizes.n_s))
+
+
+def test_cow_sources():
+    # chunk lengths 40 and 20 with k = 4: chunk 1's first block keeps 12 cached rows -> COW
+    reqs = [el.Request([40, 20], [[0, 1, 2], [3, 4]], 5, 4)]
+    cfg, sizes, v, free = _plan(reqs, 5)
+    assert sizes.n_private == 2
+    assert v["priv_src"].tolist() == [3, -1]           # COW from chunk 1 block 0; suffix block is fresh
+    assert v["priv_rows"][:16].tolist() == [0, 1, 2, 3] + [-1] * 12
+    # k = 16 recomputes the whole first block of chunk 1 (no copy), k = 20 all of chunk 1
+    for k, srcs in [(16, [-1, -1]), (20, [-1, -1, -1])]:
+        reqs = [el.Request([40, 20], [[0, 1, 2], [3, 4]], 5, k)]
+        cfg, sizes, v, free = _plan(reqs, 5)
+        assert v["priv_src"].tolist() == srcs
+
+
+def test_work_items_cover_causal_ranges():
+    rng = np.random.default_rng(9)
+    reqs, n_used = _random_requests(rng, 3, max_chunks=8, max_len=300)
+    for split in (0, 4, 16):
+        cfg, sizes, v, _ = _plan(reqs, n_used, 32, 8, split=split)
+        R = 128 // 4
+        tiles = v["tiles"].reshape(-1, 4)
+        work = v["work"].reshape(-1, 4)
+        # tiles cover S in order with at most R rows each
+        assert tiles[:, 0].tolist() == sorted(tiles[:, 0].tolist())
+        assert np.all(tiles[:, 1] >= 1) and np.all(tiles[:, 1] <= R)
+        assert int(tiles[:, 1].sum()) == sizes.n_s
+        parts = []
+        for t, (row0, nrows, p0, ns) in enumerate(tiles):
+            req = int(v["s_req"][row0])
+            last = int(v["s_pos"][row0 + nrows - 1])
+            b0 = int(v["blk_off"][req])
+            pos0 = v["block_pos0"][b0:int(v["blk_off"][req + 1])]
+            need = int(np.sum(pos0 <= last))
+            items = work[work[:, 0] == t]
+            assert len(items) == ns
+            got = sorted((int(a), int(b)) for _, a, b, _ in items)
+            assert got[0][0] == b0 and got[-1][1] == b0 + need
+            assert all(x[1] == y[0] for x, y in zip(got, got[1:]))
+            if ns == 1:
+                assert items[0, 3] == -1 and p0 == -1
+            else:
+                parts += items[:, 3].tolist()
+                assert sorted(items[:, 3].tolist()) == list(range(p0, p0 + ns))
+        assert sorted(parts) == list(range(sizes.n_partials))
+
+
+def test_empty_and_suffix_only():
+    cfg = el.attn_cfg(8, 8, 64)
+    sizes, _, v = el.epic_plan_link([el.Request([30], [[0, 1]], 0, 4)], cfg, [2, 3], 4)
+    assert sizes.n_s == 0 and sizes.n_work == 0 and sizes.n_private == 0
+    sizes, _, v = el.epic_plan_link([el.Request([], [], 20, 4)], cfg, [5, 6, 7], 8)
+    assert v["s_pos"].tolist() == list(range(20)) and sizes.n_private == 2
+
+
+@pytest.mark.parametrize("bad,status", [
+    (dict(hq=6, hkv=4), el.EpicError),
+    (dict(hq=24, hkv=8), el.EpicError),
+    (dict(d=96), el.EpicError),
+])
+def test_unsupported_shapes(bad, status):
+    a = dict(hq=8, hkv=8, d=64)
+    a.update(bad)
+    cfg = el.attn_cfg(a["hq"], a["hkv"], a["d"])
+    with pytest.raises(status) as e:
+        el.epic_plan_sizes_get([el.Request([10], [[0]], 2, 1)], cfg, 10)
+    assert e.value.status in (1, 2)
+
+
+def test_argument_errors():
+    cfg = el.attn_cfg(8, 8, 64)
+    with pytest.raises(el.EpicError) as e:                       # wrong number of blocks for a chunk
+        el.epic_plan_sizes_get([el.Request([40], [[0, 1]], 2, 1)], cfg, 10)
+    assert e.value.status == 1
+    with pytest.raises(el.EpicError) as e:                       # free block reused as chunk block
+        el.epic_plan_link([el.Request([10], [[0]], 2, 1)], cfg, [0], 4)
+    assert e.value.status == 1
+    with pytest.raises(el.EpicError) as e:                       # free list too short
+        el.epic_plan_link([el.Request([10], [[0]], 40, 1)], cfg, [1, 2], 4)
+    assert e.value.status == 3
+    with pytest.raises(el.EpicError) as e:                       # block id out of range
+        el.epic_plan_link([el.Request([10], [[7]], 2, 1)], cfg, [1], 4)
+    assert e.value.status == 1
+    with pytest.raises(el.EpicError) as e:                       # zero-length chunk
+        el.epic_plan_sizes_get([el.Request([0], [[]], 2, 1)], cfg, 10)
+    assert e.value.status == 1
+
+
+def test_repeated_chunk_in_request():
+    """The same shared chunk may appear twice in one request (read-only blocks)."""
+    cfg = el.attn_cfg(8, 8, 64)
+    reqs = [el.Request([20, 20], [[0, 1], [0, 1]], 3, 2)]
+    sizes, _, v = el.epic_plan_link(reqs, cfg, [2, 3], 4)
+    assert v["linked_blocks"].tolist() == [0, 1, 2, 1, 3]
+    assert v["priv_src"].tolist() == [0, -1]
