@@ -1,0 +1,238 @@
+#!/usr/bin/env python3
+"""Benchmark of the LegoLink link step on one MI355X.
+
+Default workload: the long-context link step -- 64 cached chunks x 2048 tokens
+(131 072 linked tokens) + 256 suffix tokens, LegoLink-32 (the first 32 tokens
+of chunks 1..63 and the suffix are recomputed: |S| = 2272 rows), GQA 32 query /
+8 KV heads, head_dim 128, bf16 KV in 16-token paged blocks.  One step = one
+call of epic_link_attention: build the private blocks (copy-on-write + write of
+the recomputed K/V), scattered-query causal attention over the linked cache,
+split-KV combine.  Inputs are resident in HBM before the timed region.
+
+Prints ONE JSON line on stdout.  value = recomputed tokens / s (|S| / step
+time); ms_per_step = link-step time (TTFT of this layer); roofline = the
+attention kernel's algorithmic TFLOP/s (4 Hq D sum(p+1) per launch) against the
+bf16 dense MFMA peak, timed with HIP events recorded around that kernel on its
+stream inside the timed region; cpu_baseline = the float64 CPU oracle on a
+sample of S rows, scaled by algorithmic flops.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "link-step TTFT (ms) + recomputed tokens/s; attention TFLOP/s vs MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA, published
+PEAK_HBM_GBS = 8000.0
+WORKLOADS = {
+    "c5k32": ("c5", {"k": 32}),
+    "c5k4": ("c5", {"k": 4}),
+    "c5k0": ("c5", {"k": 0}),
+    "c5all": ("c5", {"k": -1}),
+    "c4": ("c4", {}),
+    "c2": ("c2", {}),
+    "c1": ("c1", {}),
+}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("attention.hip", "device_common.h", "kernels.h"):
+        with open(os.path.join(ROOT, "paper_2410_15332_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(workload: str):
+    """HBM bytes per attention launch from a committed rocprofv3 --pmc summary, if it
+    was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"link_attention_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    s = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    if not m or not s or s.group(1) != kernel_source_hash():
+        return None
+    return float(m.group(1))
+
+
+def cpu_baseline(st, n_rows: int, seed: int = 1):
+    """Time the float64 oracle on a seeded sample of S rows; scale to tokens/s by flops."""
+    import numpy as np
+
+    import oracle
+    import synth
+    from threadpoolctl import threadpool_info
+
+    wl = st.wl
+    r = 0
+    lens = [wl.chunk_lens[c] for c in wl.requests[r]]
+    a, b = int(st.views["s_off"][r]), int(st.views["s_off"][r + 1])
+    s_pos = st.views["s_pos"][a:b].astype(np.int64)
+    rows = np.sort(np.random.default_rng(seed).choice(len(s_pos), size=min(n_rows, len(s_pos)), replace=False))
+    f = lambda x: synth.bf16_bits_to_f32(x).astype(np.float64)  # noqa: E731
+    ck, cv = [], []
+    for c in wl.requests[r]:
+        kb, vb = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], wl.num_kv_heads, wl.head_dim, wl.value_scale)
+        ck.append(f(kb))
+        cv.append(f(vb))
+    q, k, v = (f(x) for x in synth.row_qkv(wl.seed, r, s_pos, wl.num_q_heads, wl.num_kv_heads, wl.head_dim,
+                                            wl.value_scale))
+    t0 = time.perf_counter()
+    oracle.link_attention(lens, wl.suffix_lens[r], wl.k, ck, cv, q, k, v, rows=rows)
+    dt = time.perf_counter() - t0
+    all_pos = st.views["s_pos"].astype(np.int64)
+    f_total = float(np.sum(all_pos + 1))
+    f_sample = float(np.sum(s_pos[rows] + 1))
+    est_total_s = dt * f_total / f_sample
+    cores = max([x.get("num_threads", 1) for x in threadpool_info() if x.get("user_api") == "blas"] or [1])
+    return {
+        "value": round(len(all_pos) / est_total_s, 3),
+        "unit": "recomputed tokens/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"{len(rows)} of {len(all_pos)} S rows of request 0 (seeded uniform), float64 NumPy oracle "
+                   f"incl. K/V expansion, {dt:.1f} s; tokens/s scaled by algorithmic flops sum(p+1) "
+                   f"({f_sample:.3e} of {f_total:.3e})"),
+        "sample_seconds": round(dt, 2),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c5k32", choices=sorted(WORKLOADS))
+    ap.add_argument("--split-blocks", type=int, default=0, help="override the planner's split-KV size")
+    ap.add_argument("--cpu-rows", type=int, default=192, help="S rows in the CPU-oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="before the timed region, run one device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the link step is built and timed on a single MI355X; "
+              "multi-GPU sharding is described in DESIGN.md but not built. Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2410_15332_amd import epic_link as el
+    from paper_2410_15332_amd import harness
+    from synth.configs import get_config
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    name, kw = WORKLOADS[args.workload]
+    wl = get_config(name, **kw)
+    t0 = time.time()
+    st = harness.stage_attention(wl, device="cuda", split_blocks=args.split_blocks)
+    torch.cuda.synchronize()
+    log(f"staged {wl.name}: n_s={st.sizes.n_s} tiles={st.sizes.n_tiles} work={st.sizes.n_work} "
+        f"partials={st.sizes.n_partials} in {time.time() - t0:.1f}s")
+    flops = harness.attention_flops(st.views, wl.num_q_heads, wl.head_dim)
+
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"calibration copy of {args.calibrate_copy_mib} MiB done")
+
+    for _ in range(args.warmup):
+        st.run()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for e in (x for row in ev for x in row):   # torch creates the HIP event on its first record
+        e.record()
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    start.record()
+    for i in range(K):
+        el.epic_set_profile_events(ev[i])
+        st.run()
+    end.record()
+    el.epic_set_profile_events(None)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    step_ms = start.elapsed_time(end) / K
+    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    comb_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
+    write_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    n_s = st.sizes.n_s
+    achieved = flops / (attn_ms * 1e-3) / 1e12
+    log(f"step {step_ms:.4f} ms (wall {wall / K * 1e3:.4f} ms): write {write_ms:.4f} attn {attn_ms:.4f} "
+        f"combine {comb_ms:.4f}; attention {achieved:.1f} TFLOP/s")
+
+    traffic = traffic_from_profile(args.workload)
+    result = {
+        "metric": METRIC,
+        "value": round(n_s / (step_ms * 1e-3), 1),
+        "unit": "recomputed tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 chunk caches and recomputed q/k/v)",
+        "config": {
+            "workload": wl.name,
+            "chunks": len(wl.requests[0]) if wl.batch == 1 else [len(r) for r in wl.requests][0],
+            "batch": wl.batch,
+            "chunk_len": wl.chunk_lens[0],
+            "suffix_len": wl.suffix_lens[0],
+            "k": wl.k,
+            "num_q_heads": wl.num_q_heads,
+            "num_kv_heads": wl.num_kv_heads,
+            "head_dim": wl.head_dim,
+            "block_size": 16,
+            "recomputed_rows": n_s,
+            "linked_tokens": int(st.sizes.max_pos),
+            "parallelism": "single GPU",
+        },
+        "ttft_ms": round(step_ms, 5),
+        "attention_tflops": round(achieved, 2),
+        "attention_incl_combine_tflops": round(flops / ((attn_ms + comb_ms) * 1e-3) / 1e12, 2),
+        "kernel_ms": {"link_write": round(write_ms, 5), "attention": round(attn_ms, 5),
+                      "combine": round(comb_ms, 5)},
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "link_attention_kernel<128>",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "algorithmic_flops_per_launch": flops,
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample of S rows ...")
+        result["cpu_baseline"] = cpu_baseline(st, args.cpu_rows)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

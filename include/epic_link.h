@@ -175,6 +175,15 @@ epic_status epic_link_attention(const epic_attn_cfg* cfg, const epic_plan_sizes*
                                 uint16_t* out, float* lse,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* Profiling hook for callers that time the step's kernels.  events: NULL (off)
+ * or 4 hipEvent_t created by the caller; each entry may be NULL.  Until the
+ * next call on the same thread, every device entry point records, on its
+ * stream, events[0] before the link write, events[1] before the attention
+ * kernel, events[2] after it and events[3] after the split-KV combine (per
+ * layer for the model entry points; each record overwrites the previous one).
+ * Never fails. */
+epic_status epic_set_profile_events(void* const* events);
+
 /* ---------------------------------------------------------------- model level */
 
 /* Llama-style decoder (Sec. 5.1 models): pre-norm RMSNorm, rotary embedding

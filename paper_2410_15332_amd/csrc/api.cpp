@@ -36,6 +36,13 @@ epic_status check_plan(const epic_plan_sizes* s, const epic_plan* p) {
   return EPIC_OK;
 }
 
+// Optional profiling events of the calling thread (see epic_set_profile_events).
+thread_local hipEvent_t g_prof_events[4] = {nullptr, nullptr, nullptr, nullptr};
+
+void record_event(int i, hipStream_t stream) {
+  if (g_prof_events[i]) (void)hipEventRecord(g_prof_events[i], stream);
+}
+
 epic_status hip_status(const char* what) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(EPIC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -43,6 +50,12 @@ epic_status hip_status(const char* what) {
 }
 
 }  // namespace
+
+extern "C" epic_status epic_set_profile_events(void* const* events) {
+  clear_error();
+  for (int i = 0; i < 4; ++i) g_prof_events[i] = events ? static_cast<hipEvent_t>(events[i]) : nullptr;
+  return EPIC_OK;
+}
 
 extern "C" size_t epic_link_workspace_bytes(const epic_attn_cfg* cfg, const epic_plan_sizes* sizes) {
   if (!cfg || !sizes || validate_attn_cfg(cfg) != EPIC_OK) return 0;
@@ -57,6 +70,7 @@ epic_status run_link_attention(const epic_attn_cfg* cfg, const epic_plan_sizes* 
                                uint16_t* k_cache, uint16_t* v_cache, uint16_t* out, float* lse,
                                void* workspace, void* stream_ptr) {
   hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  record_event(0, stream);
   launch_link_write(p, s->n_private, cfg->num_kv_heads, cfg->head_dim, k_s, v_s, k_cache, v_cache, stream);
   AttnArgs a{};
   a.s_pos = p->s_pos;
@@ -80,7 +94,11 @@ epic_status run_link_attention(const epic_attn_cfg* cfg, const epic_plan_sizes* 
   a.rows_per_tile = kTileRows / a.G;
   const float scale = cfg->softmax_scale > 0.0f ? cfg->softmax_scale : 1.0f / std::sqrt(float(cfg->head_dim));
   a.scale_log2 = scale * kLog2eHost;
-  launch_link_attention(a, cfg->head_dim, s->n_work, s->n_tiles, s->n_partials, stream);
+  record_event(1, stream);
+  launch_link_attention(a, cfg->head_dim, s->n_work, stream);
+  record_event(2, stream);
+  if (s->n_partials > 0) launch_link_combine(a, cfg->head_dim, s->n_tiles, stream);
+  record_event(3, stream);
   return hip_status("link attention launch");
 }
 

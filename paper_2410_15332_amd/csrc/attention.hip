@@ -338,18 +338,22 @@ __global__ __launch_bounds__(kThreads) void link_combine_kernel(AttnArgs a) {
 
 }  // namespace
 
-void launch_link_attention(const AttnArgs& a, int head_dim, int n_work, int n_tiles, int n_partials,
-                           hipStream_t stream) {
+void launch_link_attention(const AttnArgs& a, int head_dim, int n_work, hipStream_t stream) {
   if (n_work == 0) return;
   const dim3 grid(unsigned(n_work) * unsigned(a.hkv));
-  const dim3 cgrid(unsigned(n_tiles) * unsigned(a.hkv));
-  if (head_dim == 128) {
+  if (head_dim == 128)
     link_attention_kernel<128><<<grid, kThreads, 0, stream>>>(a);
-    if (n_partials > 0) link_combine_kernel<128><<<cgrid, kThreads, 0, stream>>>(a);
-  } else {
+  else
     link_attention_kernel<64><<<grid, kThreads, 0, stream>>>(a);
-    if (n_partials > 0) link_combine_kernel<64><<<cgrid, kThreads, 0, stream>>>(a);
-  }
+}
+
+void launch_link_combine(const AttnArgs& a, int head_dim, int n_tiles, hipStream_t stream) {
+  if (n_tiles == 0) return;
+  const dim3 grid(unsigned(n_tiles) * unsigned(a.hkv));
+  if (head_dim == 128)
+    link_combine_kernel<128><<<grid, kThreads, 0, stream>>>(a);
+  else
+    link_combine_kernel<64><<<grid, kThreads, 0, stream>>>(a);
 }
 
 }  // namespace epic

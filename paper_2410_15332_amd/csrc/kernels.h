@@ -32,8 +32,9 @@ struct AttnArgs {
   float scale_log2;         // softmax scale * log2(e)
 };
 
-// Scattered-query causal attention over the paged linked cache + split-KV combine.
-void launch_link_attention(const AttnArgs& a, int head_dim, int n_work, int n_tiles, int n_partials,
-                           hipStream_t stream);
+// Scattered-query causal attention over the paged linked cache.
+void launch_link_attention(const AttnArgs& a, int head_dim, int n_work, hipStream_t stream);
+// Merge split-KV partials (tiles whose key range spans several work items).
+void launch_link_combine(const AttnArgs& a, int head_dim, int n_tiles, hipStream_t stream);
 
 }  // namespace epic

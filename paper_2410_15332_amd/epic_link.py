@@ -92,6 +92,7 @@ _link_attention = _proto("epic_link_attention", C.c_int,
                          [_P(epic_attn_cfg), _P(epic_plan_sizes), _P(epic_plan), C.c_void_p, C.c_void_p,
                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
                           C.c_void_p])
+_set_prof = _proto("epic_set_profile_events", C.c_int, [C.c_void_p])
 _model_ws = _proto("epic_model_workspace_bytes", C.c_size_t, [_P(epic_model_cfg), _P(epic_plan_sizes)])
 _link_layer = _proto("epic_link_layer", C.c_int,
                      [_P(epic_model_cfg), _P(epic_layer_weights), _P(epic_plan_sizes), _P(epic_plan), C.c_void_p,
@@ -102,8 +103,8 @@ _link_model = _proto("epic_link_model", C.c_int,
                       C.c_void_p])
 
 EXPORTED = ["epic_status_string", "epic_last_error", "epic_version", "epic_plan_sizes_get", "epic_plan_layout",
-            "epic_plan_link", "epic_link_workspace_bytes", "epic_link_attention", "epic_model_workspace_bytes",
-            "epic_link_layer", "epic_link_model"]
+            "epic_plan_link", "epic_link_workspace_bytes", "epic_link_attention", "epic_set_profile_events",
+            "epic_model_workspace_bytes", "epic_link_layer", "epic_link_model"]
 
 
 def _check(st: int, where: str):
@@ -230,6 +231,20 @@ def epic_link_attention(cfg: epic_attn_cfg, dplan: DevicePlan, q_s, k_s, v_s, k_
     _check(_link_attention(C.byref(cfg), C.byref(dplan.sizes), C.byref(dplan.plan), _ptr(q_s), _ptr(k_s),
                            _ptr(v_s), _ptr(k_cache), _ptr(v_cache), _ptr(out), _ptr(lse), _ptr(workspace),
                            ws_bytes, _stream(stream)), "epic_link_attention")
+
+
+def epic_set_profile_events(events=None):
+    """events: None, or 4 torch.cuda.Event (or None entries) recorded around the step's kernels.
+
+    torch creates an event's HIP handle on its first record(); record each event once beforehand."""
+    if events is None:
+        _check(_set_prof(None), "epic_set_profile_events")
+        return
+    handles = [None if e is None else e.cuda_event for e in events]
+    if any(h == 0 for h in handles):
+        raise ValueError("epic_set_profile_events: an event has no HIP handle yet (record it once first)")
+    arr = (C.c_void_p * 4)(*handles)
+    _check(_set_prof(C.cast(arr, C.c_void_p)), "epic_set_profile_events")
 
 
 def epic_model_workspace_bytes(cfg: epic_model_cfg, sizes: epic_plan_sizes) -> int:
