@@ -86,11 +86,12 @@ def cpu_baseline(st, n_rows: int, seed: int = 1):
     f = lambda x: synth.bf16_bits_to_f32(x).astype(np.float64)  # noqa: E731
     ck, cv = [], []
     for c in wl.requests[r]:
-        kb, vb = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], wl.num_kv_heads, wl.head_dim, wl.value_scale)
+        kb, vb = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], wl.num_kv_heads, wl.head_dim, wl.value_scale,
+                                   qk_scale=wl.qk_scale)
         ck.append(f(kb))
         cv.append(f(vb))
     q, k, v = (f(x) for x in synth.row_qkv(wl.seed, r, s_pos, wl.num_q_heads, wl.num_kv_heads, wl.head_dim,
-                                            wl.value_scale))
+                                            wl.value_scale, wl.qk_scale))
     t0 = time.perf_counter()
     oracle.link_attention(lens, wl.suffix_lens[r], wl.k, ck, cv, q, k, v, rows=rows)
     dt = time.perf_counter() - t0

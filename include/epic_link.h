@@ -115,7 +115,8 @@ typedef struct {
  *   priv_src[n_private]   shared block copied into it first, or -1
  *   priv_rows[n_private * block_size]  S row stored in each slot, or -1
  *   tiles[n_tiles * 4]    (first S row, S rows, first partial or -1, splits)
- *   work[n_work * 4]      (tile, first linked block, end linked block, partial or -1)
+ *   work[n_work * 8]      (tile, first linked block, end linked block, partial or -1,
+ *                         leading 4-block KV tiles that need no mask, 0, 0, 0)
  */
 typedef struct {
   int32_t* s_pos;

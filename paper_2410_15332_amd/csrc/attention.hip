@@ -25,6 +25,7 @@
 // rescaled only when some row's maximum grew; accumulation is fp32.
 #include "device_common.h"
 #include "kernels.h"
+#include "plan_internal.h"
 
 namespace epic {
 
@@ -55,6 +56,16 @@ __device__ __forceinline__ int srow_key(int rho) {
   return (rho >> 4) * 16 + ((rho >> 2) & 1) * 8 + ((rho >> 3) & 1) * 4 + (rho & 3);
 }
 
+// Both halves of the wavefront exchange: lane l gets op(x[l], x[l ^ 32]).
+__device__ __forceinline__ float xhalf_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xhalf_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a) {
   constexpr int NDS = D / 16;                 // k-steps of S^T = K Q^T
@@ -66,10 +77,12 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   const int hkv = a.hkv;
   const int g = blockIdx.x % hkv;
   const int item = blockIdx.x / hkv;
-  const int tile = a.work[4 * item + 0];
-  const int b0 = a.work[4 * item + 1];
-  const int b1 = a.work[4 * item + 2];
-  const int part = a.work[4 * item + 3];
+  const int32_t* wk = a.work + kWorkInts * item;
+  const int tile = wk[0];
+  const int b0 = wk[1];
+  const int b1 = wk[2];
+  const int part = wk[3];
+  const int n_fast = wk[4];                    // leading KV tiles that need no mask
   const int row0 = a.tiles[4 * tile + 0];
   const int nrows = a.tiles[4 * tile + 1];
   const int32_t* __restrict__ lblk = a.linked_blocks;
@@ -85,7 +98,6 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   const bool row_ok = srl < nrows;
   const int srow = row0 + (row_ok ? srl : nrows - 1);
   const int qpos = a.s_pos[srow];
-  const int min_qpos = a.s_pos[row0];          // S rows ascend within a request
 
   bf16x8 qreg[NDS];
   {
@@ -101,12 +113,11 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   const size_t head_k = size_t(hkv) * 16 * D;   // elements per block (all heads)
   const uint16_t* kbase = a.k_cache + size_t(g) * 16 * D;
   const uint16_t* vbase = a.v_cache + size_t(g) * 16 * D;
-  // staging registers as SSA vectors (an array here ends up in scratch memory)
+  // staging registers as SSA vectors (an array here ends up in scratch memory):
+  // kreg holds K of a tile two ahead, vreg V of the next tile
   typedef uint32_t stage_t __attribute__((ext_vector_type(4 * CH)));
   stage_t kreg, vreg;
 
-  // Global -> registers for KV tile `it`.  Block ids and lengths are uniform
-  // (scalar loads); blocks past b1 read block b1-1 and are masked later.
   // Chunk i of a thread: K key kkey0 + i*KPT (block (kkey0 + i*KPT) / 16,
   // compile-time for D = 128), 8 dims at kdc; V block vbeta0 + i*VPB, dim vd,
   // 8-slot half vhf.
@@ -114,40 +125,52 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   constexpr int VPB = kThreads / (2 * D);       // V blocks covered by one chunk index (1 or 2)
   const int kkey0 = tid / (D / 8), kdc = tid % (D / 8);
   const int vbeta0 = tid / (2 * D), vd = (tid % (2 * D)) >> 1, vhf = tid & 1;
-  auto load_tile = [&](int it) {
+
+  // Physical ids of the 4 blocks of KV tile `it` (uniform scalar loads; blocks
+  // past b1 repeat block b1-1, whose keys are masked).
+  auto tile_phys = [&](int it, int (&ph)[4]) {
     const int bb = b0 + it * 4;
-    int phys[4], len[4];
 #pragma unroll
-    for (int beta = 0; beta < 4; ++beta) {
-      const int blk = min(bb + beta, b1 - 1);
-      phys[beta] = lblk[blk];
-      len[beta] = bb + beta < b1 ? blenp[blk] : 0;
-    }
+    for (int beta = 0; beta < 4; ++beta) ph[beta] = lblk[min(bb + beta, b1 - 1)];
+  };
+  // Global -> registers: K of tile `it` (block ids ph).
+  auto load_k = [&](const int (&ph)[4]) {
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int key = kkey0 + i * KPT;
       int pb;
-      if constexpr (KPT == 16) pb = phys[i];
-      else pb = (key >> 4) == 2 * i ? phys[2 * i] : phys[2 * i + 1];
+      if constexpr (KPT == 16) pb = ph[i];
+      else pb = (key >> 4) == 2 * i ? ph[2 * i] : ph[2 * i + 1];
       const uint4 x = *reinterpret_cast<const uint4*>(kbase + size_t(pb) * head_k + (key & 15) * D + kdc * 8);
       kreg[4 * i + 0] = x.x;
       kreg[4 * i + 1] = x.y;
       kreg[4 * i + 2] = x.z;
       kreg[4 * i + 3] = x.w;
     }
+  };
+  // Global -> registers: V of tile `it`.  A masked tile zeroes V slots past each
+  // block's end, so stale or NaN bits there never meet a zero softmax weight.
+  auto load_v = [&](int it, const int (&ph)[4]) {
+    const bool fast = it < n_fast;
+    int len[4] = {16, 16, 16, 16};
+    if (!fast) {
+      const int bb = b0 + it * 4;
+#pragma unroll
+      for (int beta = 0; beta < 4; ++beta) len[beta] = bb + beta < b1 ? blenp[min(bb + beta, b1 - 1)] : 0;
+    }
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       int pb, ln;
       if constexpr (VPB == 1) {
-        pb = phys[i];
+        pb = ph[i];
         ln = len[i];
       } else {
-        pb = vbeta0 == 0 ? phys[2 * i] : phys[2 * i + 1];
+        pb = vbeta0 == 0 ? ph[2 * i] : ph[2 * i + 1];
         ln = vbeta0 == 0 ? len[2 * i] : len[2 * i + 1];
       }
       uint4 x = *reinterpret_cast<const uint4*>(vbase + size_t(pb) * head_k + vd * 16 + vhf * 8);
-      const int valid = ln - vhf * 8;            // valid slots in this 8-slot half
-      if (valid < 8) {                           // zero slots past the block's end (never NaN garbage)
+      if (!fast) {
+        const int valid = ln - vhf * 8;          // valid slots in this 8-slot half
         x.x = valid <= 0 ? 0u : valid == 1 ? (x.x & 0xFFFFu) : x.x;
         x.y = valid <= 2 ? 0u : valid == 3 ? (x.y & 0xFFFFu) : x.y;
         x.z = valid <= 4 ? 0u : valid == 5 ? (x.z & 0xFFFFu) : x.z;
@@ -159,17 +182,14 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
       vreg[4 * i + 3] = x.w;
     }
   };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i)
-      *reinterpret_cast<uint4*>(&lds.k[buf][(kkey0 + i * KPT) * KS + kdc * 8]) =
-          make_uint4(kreg[4 * i + 0], kreg[4 * i + 1], kreg[4 * i + 2], kreg[4 * i + 3]);
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int beta = vbeta0 + i * VPB;
-      *reinterpret_cast<uint4*>(&lds.v[buf][(beta * D + vd) * 16 + (vhf ^ v_swz(vd)) * 8]) =
-          make_uint4(vreg[4 * i + 0], vreg[4 * i + 1], vreg[4 * i + 2], vreg[4 * i + 3]);
-    }
+  auto store_k_chunk = [&](int buf, int i) {
+    *reinterpret_cast<uint4*>(&lds.k[buf][(kkey0 + i * KPT) * KS + kdc * 8]) =
+        make_uint4(kreg[4 * i + 0], kreg[4 * i + 1], kreg[4 * i + 2], kreg[4 * i + 3]);
+  };
+  auto store_v_chunk = [&](int buf, int i) {
+    const int beta = vbeta0 + i * VPB;
+    *reinterpret_cast<uint4*>(&lds.v[buf][(beta * D + vd) * 16 + (vhf ^ v_swz(vd)) * 8]) =
+        make_uint4(vreg[4 * i + 0], vreg[4 * i + 1], vreg[4 * i + 2], vreg[4 * i + 3]);
   };
 
   f32x16 o[NDT];
@@ -177,45 +197,75 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[dt][r] = 0.0f;
-  float m = -INFINITY, lsum = 0.0f;            // m in the scaled log2 domain
+  // Running max m (scaled log2 domain) is allowed to lag the true row max by up
+  // to kLag: the output and the sum share it, so the result is exact, P stays
+  // below 2^kLag, and O is rescaled only when some row's max jumps past it.
+  constexpr float kLag = 8.0f;
+  float m = -INFINITY, lsum = 0.0f;
   const float sl2 = a.scale_log2;
   const int krow = srow_key(col);              // K row this lane feeds into S^T
 
-  if (nkv > 0) {
-    load_tile(0);
-    store_tile(0);
+  // S^T (64 keys x 32 rows per wave) = K Q^T from LDS stage `buf`; the two
+  // 32-key subtiles alternate so that consecutive MFMAs are independent.
+  const uint16_t* kp_lane = &lds.k[0][krow * KS + half * 8];
+  auto qk = [&](int buf, f32x16 (&sc)[2]) {
+    const uint16_t* kp = kp_lane + buf * (kKT * KS);
+#pragma unroll
+    for (int q = 0; q < 2 * NDS; ++q) {
+      const int ks = q & 1, s = q >> 1;
+      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kp + ks * 32 * KS + s * 16);
+      sc[ks] = mfma_32x32x16(kf, qreg[s], s == 0 ? f32x16{} : sc[ks]);
+    }
+  };
+  // V^T operand of lane: row d = dt*32 + col, 16-byte half (half ^ swz(col)) of the row.
+  const uint16_t* vp_lane = &lds.v[0][col * 16 + (half ^ v_swz(col)) * 8];
+
+  // Software pipeline over KV tiles.  K runs one tile ahead of V: during
+  // iteration it the waves read K(it + 1) (buffer (it + 1) % 2, for S(it + 1))
+  // and V(it) (buffer it % 2), and store K(it + 2) into K buffer it % 2 and
+  // V(it + 1) into V buffer (it + 1) % 2 -- buffers nobody reads in iteration
+  // it, because their last readers ran before the barrier ending iteration
+  // it - 1.  One barrier per iteration; the stores overlap the PV MFMAs.  The
+  // MFMAs of S(it + 1) are interleaved with the exponentials of tile it.
+  int phk[4], phv[4];
+  tile_phys(0, phk);
+  load_k(phk);
+#pragma unroll
+  for (int i = 0; i < CH; ++i) store_k_chunk(0, i);
+  load_v(0, phk);
+#pragma unroll
+  for (int i = 0; i < CH; ++i) store_v_chunk(0, i);
+  if (nkv > 1) {
+    tile_phys(1, phk);
+    load_k(phk);
+#pragma unroll
+    for (int i = 0; i < CH; ++i) store_k_chunk(1, i);
+    load_v(1, phk);                            // V(1): stored during iteration 0
   }
+  tile_phys(2, phk);
+  tile_phys(2, phv);
+  if (nkv > 2) load_k(phk);                    // K(2): stored during iteration 0
+  tile_phys(3, phk);
   __syncthreads();
+
+  f32x16 sacc[2];
+  qk(0, sacc);
+  __syncthreads();                             // K buffer 0 is rewritten in iteration 0
 
   for (int it = 0; it < nkv; ++it) {
     const int cur = it & 1;
-    if (it + 1 < nkv) load_tile(it + 1);
 
-    // S^T (64 keys x 32 rows per wave) = K Q^T
-    f32x16 sacc[2];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[ks][r] = 0.0f;
-      const uint16_t* kp = &lds.k[cur][(ks * 32 + krow) * KS + half * 8];
-#pragma unroll
-      for (int s = 0; s < NDS; ++s)
-        sacc[ks] = mfma_32x32x16(*reinterpret_cast<const bf16x8*>(kp + s * 16), qreg[s], sacc[ks]);
-    }
-
-    // Mask (only tiles that reach past the first row, or hold partial blocks).
+    // Mask: only tiles past the item's unmasked prefix (diagonal, partial blocks).
     // Register r = i*4 + j of subtile ks holds key ks*32 + (i>>1)*16 + half*8 + (i&1)*4 + j.
-    const int bb = b0 + it * 4;
-    int bpos0[4], blen[4];
+    if (it >= n_fast) {
+      const int bb = b0 + it * 4;
+      int bpos0[4], blen[4];
 #pragma unroll
-    for (int beta = 0; beta < 4; ++beta) {
-      const int blk = min(bb + beta, b1 - 1);
-      bpos0[beta] = bpos[blk];
-      blen[beta] = bb + beta < b1 ? blenp[blk] : 0;
-    }
-    const bool full = blen[0] == 16 && blen[1] == 16 && blen[2] == 16 && blen[3] == 16 &&
-                      bpos0[3] + 15 <= min_qpos;
-    if (!full) {
+      for (int beta = 0; beta < 4; ++beta) {
+        const int blk = min(bb + beta, b1 - 1);
+        bpos0[beta] = bpos[blk];
+        blen[beta] = bb + beta < b1 ? blenp[blk] : 0;
+      }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
@@ -227,66 +277,105 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
           sacc[ks][r] = ok ? sacc[ks][r] : -INFINITY;
         }
     }
-    float mt = sacc[0][0];
+
+    // row max: independent partial maxima, then one lane swap across halves
+    float mx[8];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sacc[ks][r]);
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m, mt * sl2);
-    const float m_use = m_new == -INFINITY ? 0.0f : m_new;
-    if (__ballot(m_new > m)) {                 // some row's max moved: rescale
-      const float alpha = fast_exp2(m - m_use);
+    for (int c = 0; c < 8; ++c)
+      mx[c] = fmaxf(fmaxf(sacc[c >> 2][(c & 3) * 4 + 0], sacc[c >> 2][(c & 3) * 4 + 1]),
+                    fmaxf(sacc[c >> 2][(c & 3) * 4 + 2], sacc[c >> 2][(c & 3) * 4 + 3]));
+    const float mt = xhalf_max(fmaxf(fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3])),
+                                     fmaxf(fmaxf(mx[4], mx[5]), fmaxf(mx[6], mx[7]))));
+    const float m_cand = fmaxf(m, mt * sl2);
+    const bool grow = m_cand > m + kLag;       // also true on the first finite max
+    if (__ballot(grow)) {
+      const float alpha = grow ? fast_exp2(m - m_cand) : 1.0f;
+      m = grow ? m_cand : m;
       lsum *= alpha;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
     }
-    m = m_new;
-    float ls = 0.0f;
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(__builtin_fmaf(sacc[ks][r], sl2, -m_use));
-        sacc[ks][r] = p;
-        ls += p;
-      }
-    lsum += ls;
+    const float m_use = m == -INFINITY ? 0.0f : m;
 
-    // P^T as bf16 B operands: registers 8st .. 8st+7 of subtile ks = keys ks*32 + st*16 + half*8 + [0, 8).
-    bf16x8 pb[2][2];
+    // Exponentials of tile it, interleaved with the S(it + 1) MFMAs.
+    f32x16 snext[2];
+    uint32_t pw[16];                           // P(it) packed to bf16 pairs
+    float ps[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    auto softmax_step = [&](int q) {
+      constexpr int VPS = 32 / (2 * NDS);      // scores per MFMA step
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        const int r0 = st * 8;
-        uint4 u = make_uint4(pack_bf16x2(sacc[ks][r0 + 0], sacc[ks][r0 + 1]),
-                             pack_bf16x2(sacc[ks][r0 + 2], sacc[ks][r0 + 3]),
-                             pack_bf16x2(sacc[ks][r0 + 4], sacc[ks][r0 + 5]),
-                             pack_bf16x2(sacc[ks][r0 + 6], sacc[ks][r0 + 7]));
-        pb[ks][st] = __builtin_bit_cast(bf16x8, u);
+      for (int v = 0; v < VPS; ++v) {
+        const int idx = q * VPS + v;           // flattened register (ks = idx / 16, r = idx % 16)
+        const float p = fast_exp2(__builtin_fmaf(sacc[idx >> 4][idx & 15], sl2, -m_use));
+        sacc[idx >> 4][idx & 15] = p;
+        ps[idx & 3] += p;
+        if (idx & 1) pw[idx >> 1] = pack_bf16x2(sacc[idx >> 4][(idx & 15) - 1], p);
       }
+    };
+    if (it + 1 < nkv) {
+      const uint16_t* kp = kp_lane + (cur ^ 1) * (kKT * KS);
+      bf16x8 kf[2];                            // K fragments, read one step ahead
+      kf[0] = *reinterpret_cast<const bf16x8*>(kp);
+#pragma unroll
+      for (int q = 0; q < 2 * NDS; ++q) {
+        const int ks = q & 1, s = q >> 1;
+        if (q + 1 < 2 * NDS)
+          kf[(q + 1) & 1] = *reinterpret_cast<const bf16x8*>(kp + ((q + 1) & 1) * 32 * KS + ((q + 1) >> 1) * 16);
+        snext[ks] = mfma_32x32x16(kf[q & 1], qreg[s], s == 0 ? f32x16{} : snext[ks]);
+        softmax_step(q);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 2 * NDS; ++q) softmax_step(q);
+    }
+    lsum += (ps[0] + ps[1]) + (ps[2] + ps[3]);
 
-    // O^T (D x 32 rows) += V^T (D x 64 keys) P^T: one 16-byte LDS read per MFMA.
+    // O^T (D x 32 rows) += V^T (D x 64 keys) P^T.  B operand of step (ks, st) =
+    // keys ks*32 + st*16 + half*8 + [0, 8) = packed words 8ks + 4st .. +3; the
+    // V^T operand is one 16-byte LDS read; the D/32 accumulators alternate.
+    const uint16_t* vp = vp_lane + cur * (4 * D * 16);
+    const bool st_k = it + 2 < nkv, st_v = it + 1 < nkv;
+    bf16x8 vf[2];                              // V^T fragments, read one MFMA ahead
+    vf[0] = *reinterpret_cast<const bf16x8*>(vp);
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
-      const int d = dt * 32 + col;
-      const uint16_t* vp = &lds.v[cur][d * 16 + (half ^ v_swz(d)) * 8];
+    for (int kst = 0; kst < 4; ++kst) {
+      const bf16x8 pbk = __builtin_bit_cast(
+          bf16x8, make_uint4(pw[4 * kst + 0], pw[4 * kst + 1], pw[4 * kst + 2], pw[4 * kst + 3]));
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-          o[dt] = mfma_32x32x16(*reinterpret_cast<const bf16x8*>(vp + (ks * 2 + st) * D * 16), pb[ks][st],
-                                o[dt]);
+      for (int dt = 0; dt < NDT; ++dt) {
+        const int n = kst * NDT + dt + 1;      // next fragment
+        if (n < 4 * NDT)
+          vf[n & 1] = *reinterpret_cast<const bf16x8*>(vp + (n / NDT) * D * 16 + (n % NDT) * 32 * 16);
+        o[dt] = mfma_32x32x16(vf[(n - 1) & 1], pbk, o[dt]);
+        // LDS stores of K(it + 2) and V(it + 1), spread over the PV MFMAs
+        const int c = n - 1;
+        if (c < CH) {
+          if (st_k) store_k_chunk(cur, c);
+        } else if (c < 2 * CH) {
+          if (st_v) store_v_chunk(cur ^ 1, c - CH);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // next global loads: K(it + 3), V(it + 2)
+    if (it + 3 < nkv) load_k(phk);
+    tile_phys(it + 4, phk);
+    if (it + 2 < nkv) {
+      tile_phys(it + 2, phv);
+      load_v(it + 2, phv);
     }
 
-    if (it + 1 < nkv) store_tile(cur ^ 1);
-    __syncthreads();
+    if (it + 1 < nkv) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) sacc[ks] = snext[ks];
+      __syncthreads();                         // stores of this iteration visible; buffers free
+    }
   }
 
-  const float ltot = lsum + __shfl_xor(lsum, 32);
+  const float ltot = xhalf_sum(lsum);
   if (!row_ok) return;
   const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
   if (part < 0) {

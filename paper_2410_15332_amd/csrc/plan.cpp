@@ -201,7 +201,7 @@ extern "C" epic_status epic_plan_sizes_get(const epic_link_request* reqs, int32_
   s.n_partials = static_cast<int32_t>(n_part);
   s.max_pos = static_cast<int32_t>(max_pos);
   s.total_ints = 3 * align16(n_s) + 2 * align16(batch + 1) + 3 * align16(n_lb) + 2 * align16(n_priv) +
-                 align16(n_priv * kBlock) + align16(4 * int64_t(tiles.size())) + align16(4 * n_work);
+                 align16(n_priv * kBlock) + align16(4 * int64_t(tiles.size())) + align16(kWorkInts * n_work);
   *out = s;
   return EPIC_OK;
 }
@@ -227,7 +227,7 @@ extern "C" epic_status epic_plan_layout(const epic_plan_sizes* s, int32_t* base,
   p->priv_src = take(s->n_private);
   p->priv_rows = take(int64_t(s->n_private) * kBlock);
   p->tiles = take(4 * int64_t(s->n_tiles));
-  p->work = take(4 * int64_t(s->n_work));
+  p->work = take(kWorkInts * int64_t(s->n_work));
   if (cur - base != s->total_ints) return fail(EPIC_ERR_INVALID_ARG, "plan sizes are inconsistent");
   return EPIC_OK;
 }
@@ -363,10 +363,25 @@ extern "C" epic_status epic_plan_link(const epic_link_request* reqs, int32_t bat
       const int base = plan->blk_off[tiles[t].req];
       const int b0 = base + seg * split;
       const int b1 = base + std::min(tiles[t].nblk, (seg + 1) * split);
-      plan->work[4 * w + 0] = static_cast<int32_t>(t);
-      plan->work[4 * w + 1] = b0;
-      plan->work[4 * w + 2] = b1;
-      plan->work[4 * w + 3] = ns > 1 ? plan->tiles[4 * t + 2] + seg : -1;
+      // Leading KV tiles (kKvTileBlocks blocks each) that need no mask: all
+      // blocks full and every key at or before the tile's first row.
+      const int32_t first_pos = plan->s_pos[tiles[t].row0];
+      int n_fast = 0;
+      for (int b = b0; b + kKvTileBlocks <= b1; b += kKvTileBlocks) {
+        bool ok = true;
+        for (int i = 0; i < kKvTileBlocks; ++i) ok = ok && plan->block_len[b + i] == kBlock;
+        const int last = b + kKvTileBlocks - 1;
+        ok = ok && plan->block_pos0[last] + kBlock - 1 <= first_pos;
+        if (!ok) break;
+        ++n_fast;
+      }
+      int32_t* wk = plan->work + int64_t(kWorkInts) * w;
+      wk[0] = static_cast<int32_t>(t);
+      wk[1] = b0;
+      wk[2] = b1;
+      wk[3] = ns > 1 ? plan->tiles[4 * t + 2] + seg : -1;
+      wk[4] = n_fast;
+      wk[5] = wk[6] = wk[7] = 0;
       ++w;
     }
   }

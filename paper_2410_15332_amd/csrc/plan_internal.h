@@ -8,6 +8,7 @@ namespace epic {
 constexpr int kBlock = 16;         // token slots per KV block
 constexpr int kTileRows = 128;     // (S row, query head) pairs per attention tile
 constexpr int kKvTileBlocks = 4;   // KV blocks staged per attention iteration (64 keys)
+constexpr int kWorkInts = 8;       // int32 per attention work item
 constexpr float kLog2eHost = 1.442695040888963407f;
 
 epic_status validate_attn_cfg(const epic_attn_cfg* cfg);

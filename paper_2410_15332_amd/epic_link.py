@@ -18,6 +18,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libepic_li
 
 EPIC_OK = 0
 BLOCK = 16
+WORK_INTS = 8     # int32 per attention work item in the plan
 
 
 class EpicError(RuntimeError):
@@ -188,7 +189,7 @@ def plan_views(sizes: epic_plan_sizes, buf: np.ndarray) -> dict:
             "linked_blocks": sizes.n_linked_blocks, "block_pos0": sizes.n_linked_blocks,
             "block_len": sizes.n_linked_blocks, "blk_off": sizes.batch + 1, "priv_block": sizes.n_private,
             "priv_src": sizes.n_private, "priv_rows": sizes.n_private * BLOCK, "tiles": 4 * sizes.n_tiles,
-            "work": 4 * sizes.n_work}
+            "work": WORK_INTS * sizes.n_work}
     out = {}
     for name in PLAN_FIELDS:
         addr = C.cast(getattr(plan, name), C.c_void_p).value or base

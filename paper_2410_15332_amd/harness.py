@@ -97,7 +97,7 @@ def stage_attention(wl: AttnWorkload, device="cuda", split_blocks: int = 0, spar
     vpool = np.zeros((num_blocks, hkv, d, el.BLOCK), np.uint16)
 
     def fill(c):
-        kr, vr = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], hkv, d, wl.value_scale)
+        kr, vr = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], hkv, d, wl.value_scale, qk_scale=wl.qk_scale)
         kb, vb = el.pack_blocks(kr, vr)
         kpool[block_of[c]] = kb
         vpool[block_of[c]] = vb
@@ -116,7 +116,8 @@ def stage_attention(wl: AttnWorkload, device="cuda", split_blocks: int = 0, spar
 
     def rows(job):
         r, a, b = job
-        q[a:b], k[a:b], v[a:b] = synth.row_qkv(wl.seed, r, s_pos[a:b], hq, hkv, d, wl.value_scale)
+        q[a:b], k[a:b], v[a:b] = synth.row_qkv(wl.seed, r, s_pos[a:b], hq, hkv, d, wl.value_scale,
+                                                wl.qk_scale)
 
     jobs = []
     for r in range(wl.batch):

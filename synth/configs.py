@@ -30,6 +30,7 @@ class AttnWorkload:
     suffix_lens: List[int]           # per request
     k: int                           # LegoLink-k; k < 0 = recompute every token (FR)
     value_scale: float = 1.0         # values are N(0,1) * value_scale
+    qk_scale: float = 1.0            # queries and keys additionally scaled by this
 
     @property
     def batch(self) -> int:

@@ -44,25 +44,27 @@ def _normal_bf16(rng: np.random.Generator, shape, scale: float) -> np.ndarray:
 
 
 def chunk_cache(seed: int, chunk_id: int, length: int, hkv: int, d: int,
-                scale: float = 1.0, layer: int = 0) -> Tuple[np.ndarray, np.ndarray]:
-    """Cached K and V of one immutable chunk, bf16 bits [length, hkv, d] each."""
+                scale: float = 1.0, layer: int = 0, qk_scale: float = 1.0) -> Tuple[np.ndarray, np.ndarray]:
+    """Cached K and V of one immutable chunk, bf16 bits [length, hkv, d] each.
+    K is N(0, 1) * scale * qk_scale, V is N(0, 1) * scale."""
     rng = np.random.default_rng([seed, _CHUNK, layer, chunk_id])
-    k = _normal_bf16(rng, (length, hkv, d), scale)
+    k = _normal_bf16(rng, (length, hkv, d), scale * qk_scale)
     v = _normal_bf16(rng, (length, hkv, d), scale)
     return k, v
 
 
 def row_qkv(seed: int, request: int, positions: Sequence[int], hq: int, hkv: int, d: int,
-            scale: float = 1.0) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
-    """q [n, hq, d], k [n, hkv, d], v [n, hkv, d] (bf16 bits) for the given linked positions."""
+            scale: float = 1.0, qk_scale: float = 1.0) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """q [n, hq, d], k [n, hkv, d], v [n, hkv, d] (bf16 bits) for the given linked positions;
+    q and k are N(0, 1) * scale * qk_scale, v is N(0, 1) * scale."""
     n = len(positions)
     q = np.empty((n, hq, d), np.uint16)
     k = np.empty((n, hkv, d), np.uint16)
     v = np.empty((n, hkv, d), np.uint16)
     for i, p in enumerate(positions):
         rng = np.random.default_rng([seed, _ROW, request, int(p)])
-        q[i] = _normal_bf16(rng, (hq, d), scale)
-        k[i] = _normal_bf16(rng, (hkv, d), scale)
+        q[i] = _normal_bf16(rng, (hq, d), scale * qk_scale)
+        k[i] = _normal_bf16(rng, (hkv, d), scale * qk_scale)
         v[i] = _normal_bf16(rng, (hkv, d), scale)
     return q, k, v
 

@@ -52,8 +52,9 @@ def _sample_rows(n, seed, n_rand=48, tile=32):
     return np.array(sorted(rows), dtype=np.int64)
 
 
-def check_stage(st, sample=None, seed=0, scaled_tol=False):
-    """scaled_tol: allow 2e-2 * max(1, |ref|) per element (values far from N(0, 1))."""
+def check_stage(st, sample=None, seed=0):
+    """The 2e-2 output bar holds for N(0, 1) values; values drawn with a larger
+    scale c are weighted averages of vectors c times larger, so the bar scales by c."""
     el = _el()
     wl = st.wl
     torch.cuda.synchronize()
@@ -70,20 +71,18 @@ def check_stage(st, sample=None, seed=0, scaled_tol=False):
         assert np.array_equal(v["s_pos"][a:b], s_ref), "planner selection differs from the oracle"
         ck, cv = [], []
         for c in chunks:
-            kb, vb = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], hkv, d, wl.value_scale)
+            kb, vb = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], hkv, d, wl.value_scale, qk_scale=wl.qk_scale)
             ck.append(_f64(kb)); cv.append(_f64(vb))
         if len(s_ref) == 0:
             continue
-        q, k, vv = (_f64(x) for x in synth.row_qkv(wl.seed, r, s_ref, hq, hkv, d, wl.value_scale))
+        q, k, vv = (_f64(x) for x in synth.row_qkv(wl.seed, r, s_ref, hq, hkv, d, wl.value_scale,
+                                                   wl.qk_scale))
         rows = None if sample is None else sample(len(s_ref), seed + r)
         _, o_ref, l_ref, K_exp, V_exp = oracle.link_attention(lens, wl.suffix_lens[r], wl.k, ck, cv, q, k, vv,
                                                               rows=rows)
         idx = np.arange(len(s_ref)) if rows is None else rows
         got = out[a + idx]
-        diff = np.abs(got - o_ref)
-        if scaled_tol:
-            diff = diff / np.maximum(1.0, np.abs(o_ref))
-        err = diff.max()
+        err = np.abs(got - o_ref).max() / max(1.0, wl.value_scale)
         worst = max(worst, err)
         assert err <= OUT_ATOL, f"request {r}: max |out err| {err}"
         gl = lse[a + idx].astype(np.float64)
@@ -96,7 +95,7 @@ def check_stage(st, sample=None, seed=0, scaled_tol=False):
         assert np.array_equal(_f64(gv), V_exp), f"request {r}: linked V differs"
     # shared chunk blocks are never written
     for c, ids in st.chunk_block_ids.items():
-        kr, vr = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], hkv, d, wl.value_scale)
+        kr, vr = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], hkv, d, wl.value_scale, qk_scale=wl.qk_scale)
         kb, vb = el.pack_blocks(kr, vr)
         assert np.array_equal(kc[ids], kb) and np.array_equal(vc[ids], vb), f"chunk {c} blocks modified"
     print(f"[gpu-test] {wl.name}: max |out err| {worst:.3e}", flush=True)
@@ -143,8 +142,8 @@ def test_c5_all_tokens_sampled():
     check_stage(st, sample=pick)
 
 
-def _wl(name, lens, reqs, suffix, k, hq, hkv, d, scale=1.0, seed=77):
-    return AttnWorkload(name, seed, hq, hkv, d, 16, reqs, lens, suffix, k, scale)
+def _wl(name, lens, reqs, suffix, k, hq, hkv, d, scale=1.0, seed=77, qk_scale=1.0):
+    return AttnWorkload(name, seed, hq, hkv, d, 16, reqs, lens, suffix, k, scale, qk_scale)
 
 
 EDGE = [
@@ -158,8 +157,11 @@ EDGE = [
     _wl("suffix_only", [], [[]], [150], 4, 32, 8, 128),
     # repeated chunk inside a request and shared across a batch, G = 2
     _wl("batch_repeat", [48, 33, 16], [[0, 1, 0], [2, 1], [1]], [5, 40, 0], 20, 8, 4, 64),
-    # large logits (values scaled by 5: |logit| up to ~100): online-softmax stability
-    _wl("large_logits", [200, 300, 150], [[0, 1, 2]], [33], 32, 32, 8, 128, scale=5.0),
+    # large logits (q and k scaled by 5: |logit| up to ~100 nats, V ~ N(0, 1)):
+    # online-softmax stability, max tracking over many tiles
+    _wl("large_logits", [200, 300, 150], [[0, 1, 2]], [33], 32, 32, 8, 128, qk_scale=5.0),
+    # moderately larger values everywhere (x3): bf16 outputs up to ~12, relative bar
+    _wl("scaled_values", [200, 300, 150], [[0, 1, 2]], [33], 32, 32, 8, 128, scale=3.0),
 ]
 
 
@@ -167,7 +169,7 @@ EDGE = [
 def test_edge_cases(wl):
     st = _stage(wl)
     st.run()
-    check_stage(st, scaled_tol=wl.value_scale > 1.0)
+    check_stage(st)
 
 
 @pytest.mark.parametrize("split", [4, 8, 36])

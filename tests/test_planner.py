@@ -100,7 +100,7 @@ def test_work_items_cover_causal_ranges():
         cfg, sizes, v, _ = _plan(reqs, n_used, 32, 8, split=split)
         R = 128 // 4
         tiles = v["tiles"].reshape(-1, 4)
-        work = v["work"].reshape(-1, 4)
+        work = v["work"].reshape(-1, el.WORK_INTS)
         # tiles cover S in order with at most R rows each
         assert tiles[:, 0].tolist() == sorted(tiles[:, 0].tolist())
         assert np.all(tiles[:, 1] >= 1) and np.all(tiles[:, 1] <= R)
@@ -114,7 +114,19 @@ def test_work_items_cover_causal_ranges():
             need = int(np.sum(pos0 <= last))
             items = work[work[:, 0] == t]
             assert len(items) == ns
-            got = sorted((int(a), int(b)) for _, a, b, _ in items)
+            got = sorted((int(it[1]), int(it[2])) for it in items)
+            for it in items:   # leading unmasked KV tiles: full blocks, all keys <= first row
+                nf = int(it[4])
+                first = int(v["s_pos"][row0])
+                for q in range(nf):
+                    bs = range(int(it[1]) + 4 * q, int(it[1]) + 4 * q + 4)
+                    assert all(v["block_len"][b] == 16 for b in bs)
+                    assert v["block_pos0"][bs[-1]] + 15 <= first
+                q = nf
+                b = int(it[1]) + 4 * q
+                if b + 4 <= int(it[2]):
+                    bs = range(b, b + 4)
+                    assert not (all(v["block_len"][x] == 16 for x in bs) and v["block_pos0"][bs[-1]] + 15 <= first)
             assert got[0][0] == b0 and got[-1][1] == b0 + need
             assert all(x[1] == y[0] for x, y in zip(got, got[1:]))
             if ns == 1:
