@@ -16,7 +16,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build", "epic_link")
 LIB = os.path.join(PKG, "libepic_link.so")
 
-SOURCES = ["status.cpp", "plan.cpp", "api.cpp", "model.cpp", "link_write.hip", "attention.hip"]
+SOURCES = ["status.cpp", "plan.cpp", "api.cpp", "model.cpp", "link_write.hip", "attention.hip", "gemm.hip",
+           "layer.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed fp32 VALU forms are disabled: hipcc must not emit them for this target.

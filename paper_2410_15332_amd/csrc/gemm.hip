@@ -1,0 +1,148 @@
+// Row-set GEMMs of the link step on MFMA: C[M x N] = A[M x K] . W[N x K]^T.
+//
+// A holds the selected rows' activations (bf16, K contiguous), W a weight
+// matrix in [out][in] layout (bf16), so both MFMA operands are read along K.
+// Epilogues are fused:
+//   kStoreF32 : C -> fp32 [M][N]                     (Q/K/V projections, Sec. 4.2)
+//   kResidual : h[M][N] += C                         (W_O and W_down; fp32 residual stream)
+//   kSwiGLU   : act[M][N/2] = silu(gate) * up, bf16  (W_gate_up; gate rows [0, F), up rows [F, 2F))
+//
+// Tiling: 256 threads = 4 wavefronts, workgroup tile 128 x 128, each wavefront
+// 64 x 64 as 2 x 2 v_mfma_f32_32x32x16_bf16 tiles, K in steps of 32 staged in
+// LDS (rows padded to 80 bytes so the 16 rows one ds_read_b128 pass touches
+// fall in distinct banks), double-buffered through registers.  For kSwiGLU the
+// 128 weight rows of a tile are gate/up in 32-row groups (gate j.., up j..,
+// gate j+32.., up j+32..), so each wavefront's two 32-column MFMA tiles hold
+// gate and up of the same 32 outputs in the same registers.
+// Rows past M are computed from a clamped row and never stored.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace epic {
+
+namespace {
+
+constexpr int kBM = 128, kBN = 128, kBK = 32;
+constexpr int kLdsRow = kBK + 8;   // elements per LDS row (80 bytes)
+constexpr int kGemmThreads = 256;
+
+template <int EPI>
+__global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) uint16_t lds_a[2][kBM * kLdsRow];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_b[2][kBN * kLdsRow];
+
+  const int m_tiles = (g.M + kBM - 1) / kBM;
+  const int mt = blockIdx.x % m_tiles;       // the M tiles of one weight tile are launched together
+  const int nt = blockIdx.x / m_tiles;
+  const int m0 = mt * kBM;
+  const int tid = threadIdx.x & (kGemmThreads - 1);
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int col = lane & 31, half = lane >> 5;
+
+  // weight row of tile column c
+  auto wrow = [&](int c) -> int {
+    if constexpr (EPI == kSwiGLU) {
+      const int grp = c >> 5;                // 0: gate, 1: up, 2: gate, 3: up
+      return (grp & 1) * g.ffn + nt * 64 + (grp >> 1) * 32 + (c & 31);
+    } else {
+      return nt * kBN + c;
+    }
+  };
+
+  // global -> register staging: 128 rows x 32 k = 512 chunks of 16 bytes per operand, 2 per thread
+  const int ld_row = tid >> 2, ld_kc = (tid & 3) * 8;        // rows ld_row and ld_row + 64
+  const uint16_t* a_ptr[2];
+  const uint16_t* b_ptr[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = ld_row + 64 * i;
+    a_ptr[i] = g.A + size_t(min(m0 + r, g.M - 1)) * g.K + ld_kc;
+    b_ptr[i] = g.W + size_t(wrow(r)) * g.K + ld_kc;
+  }
+  uint4 ra[2], rb[2];
+  auto load = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      ra[i] = *reinterpret_cast<const uint4*>(a_ptr[i] + kt * kBK);
+      rb[i] = *reinterpret_cast<const uint4*>(b_ptr[i] + kt * kBK);
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      *reinterpret_cast<uint4*>(&lds_a[buf][(ld_row + 64 * i) * kLdsRow + ld_kc]) = ra[i];
+      *reinterpret_cast<uint4*>(&lds_b[buf][(ld_row + 64 * i) * kLdsRow + ld_kc]) = rb[i];
+    }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+
+  const int nk = g.K / kBK;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) load(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      bf16x8 af[2], bfr[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        af[i] = *reinterpret_cast<const bf16x8*>(&lds_a[cur][(wm * 64 + i * 32 + col) * kLdsRow + ks * 16 + half * 8]);
+        bfr[i] = *reinterpret_cast<const bf16x8*>(&lds_b[cur][(wn * 64 + i * 32 + col) * kLdsRow + ks * 16 + half * 8]);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma_32x32x16(af[i], bfr[j], acc[i][j]);
+    }
+    if (kt + 1 < nk) store(cur ^ 1);
+    __syncthreads();
+  }
+
+  // Epilogue.  acc[i][j] register r: row wm*64 + i*32 + (r/4)*8 + half*4 + r%4, column wn*64 + j*32 + col.
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = m0 + wm * 64 + i * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+      if (m >= g.M) continue;
+      if constexpr (EPI == kSwiGLU) {
+        const float gt = acc[i][0][r], up = acc[i][1][r];
+        const float act = gt / (1.0f + __expf(-gt)) * up;
+        const int n = nt * 64 + wn * 32 + col;
+        g.act[size_t(m) * g.ffn + n] = uint16_t(pack_bf16x2(act, 0.0f) & 0xFFFFu);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int n = nt * kBN + wn * 64 + j * 32 + col;
+          if constexpr (EPI == kStoreF32)
+            g.C[size_t(m) * g.N + n] = acc[i][j][r];
+          else
+            g.C[size_t(m) * g.N + n] += acc[i][j][r];
+        }
+      }
+    }
+}
+
+}  // namespace
+
+void launch_gemm(const GemmArgs& g, int epi, hipStream_t stream) {
+  const int m_tiles = (g.M + kBM - 1) / kBM;
+  const int n_tiles = epi == kSwiGLU ? g.ffn / 64 : g.N / kBN;
+  const dim3 grid(unsigned(m_tiles) * unsigned(n_tiles));
+  if (g.M == 0) return;
+  switch (epi) {
+    case kStoreF32: gemm_kernel<kStoreF32><<<grid, kGemmThreads, 0, stream>>>(g); break;
+    case kResidual: gemm_kernel<kResidual><<<grid, kGemmThreads, 0, stream>>>(g); break;
+    default: gemm_kernel<kSwiGLU><<<grid, kGemmThreads, 0, stream>>>(g); break;
+  }
+}
+
+}  // namespace epic

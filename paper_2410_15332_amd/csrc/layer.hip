@@ -1,0 +1,129 @@
+// Elementwise parts of a decoder layer for the selected rows: RMSNorm, the
+// rotary table at linked positions, and the rotation / bf16 split of the fused
+// Q|K|V projection.
+//
+// RMSNorm: y = x / sqrt(mean(x^2) + eps) * w, fp32 statistics.
+// Rotary embedding: the pair (i, i + D/2) of a head is rotated by angle
+// pos * theta^(-2i/D), pos = the row's LINKED position (its place in the
+// concatenated sequence), so recomputed chunk tokens see their non-initial
+// positions (Sec. 4.2).  Angles are formed in float64: in float32,
+// pos * inv_freq at pos ~ 1e5 would be off by ~1e-2 rad.
+#include <cmath>
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace epic {
+
+namespace {
+
+constexpr int kNormThreads = 256;
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  float s = 0.0f;
+#pragma unroll
+  for (int w = 0; w < kNormThreads / 64; ++w) s += red[w];
+  return s;
+}
+
+// One workgroup per row; hidden % 4 == 0.  out_bf16 or out_f32 receives the row.
+__global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __restrict__ x, const uint16_t* __restrict__ w,
+                                                               uint16_t* __restrict__ out_bf16,
+                                                               float* __restrict__ out_f32, int hidden, float eps) {
+  __shared__ float red[kNormThreads / 64];
+  const int row = blockIdx.x;
+  const float4* xr = reinterpret_cast<const float4*>(x + size_t(row) * hidden);
+  float ss = 0.0f;
+  for (int i = threadIdx.x; i < hidden / 4; i += kNormThreads) {
+    const float4 v = xr[i];
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  const float total = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(total / float(hidden) + eps);
+  for (int i = threadIdx.x; i < hidden / 4; i += kNormThreads) {
+    const float4 v = xr[i];
+    const uint2 wb = *reinterpret_cast<const uint2*>(w + 4 * i);
+    const float y0 = v.x * inv * bf16_to_f32(uint16_t(wb.x & 0xFFFFu));
+    const float y1 = v.y * inv * bf16_to_f32(uint16_t(wb.x >> 16));
+    const float y2 = v.z * inv * bf16_to_f32(uint16_t(wb.y & 0xFFFFu));
+    const float y3 = v.w * inv * bf16_to_f32(uint16_t(wb.y >> 16));
+    if (out_bf16) {
+      *reinterpret_cast<uint2*>(out_bf16 + size_t(row) * hidden + 4 * i) =
+          make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+    } else {
+      *reinterpret_cast<float4*>(out_f32 + size_t(row) * hidden + 4 * i) = make_float4(y0, y1, y2, y3);
+    }
+  }
+}
+
+// cs[row][i] = (cos, sin)(s_pos[row] * theta^(-2i/D)), float64 angle.
+__global__ void rope_table_kernel(const int32_t* __restrict__ s_pos, float2* __restrict__ cs, int n_rows, int half_dim,
+                                  double log2_theta) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n_rows * half_dim) return;
+  const int row = idx / half_dim, i = idx % half_dim;
+  const double inv_freq = exp2(-double(2 * i) / double(2 * half_dim) * log2_theta);
+  const double ang = double(s_pos[row]) * inv_freq;
+  double s, c;
+  sincos(ang, &s, &c);
+  cs[idx] = make_float2(float(c), float(s));
+}
+
+// qkv fp32 [n][(hq + 2 hkv) D] -> q, k rotated, v copied, all bf16 [n][heads][D].
+// One thread per rotation pair; grid covers n * (hq + 2 hkv) * D/2 pairs.
+__global__ void rope_split_kernel(const float* __restrict__ qkv, const float2* __restrict__ cs,
+                                  uint16_t* __restrict__ q, uint16_t* __restrict__ k, uint16_t* __restrict__ v,
+                                  int n_rows, int hq, int hkv, int D) {
+  const int half = D / 2;
+  const int heads = hq + 2 * hkv;
+  const long idx = long(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= long(n_rows) * heads * half) return;
+  const int i = int(idx % half);
+  const int hd = int((idx / half) % heads);
+  const int row = int(idx / (long(half) * heads));
+  const float* src = qkv + (size_t(row) * heads + hd) * D;
+  const float x1 = src[i], x2 = src[i + half];
+  float y1 = x1, y2 = x2;
+  if (hd < hq + hkv) {                       // q and k heads rotate, v heads do not
+    const float2 t = cs[size_t(row) * half + i];
+    y1 = x1 * t.x - x2 * t.y;
+    y2 = x2 * t.x + x1 * t.y;
+  }
+  uint16_t* dst;
+  if (hd < hq)
+    dst = q + (size_t(row) * hq + hd) * D;
+  else if (hd < hq + hkv)
+    dst = k + (size_t(row) * hkv + (hd - hq)) * D;
+  else
+    dst = v + (size_t(row) * hkv + (hd - hq - hkv)) * D;
+  dst[i] = uint16_t(pack_bf16x2(y1, 0.0f) & 0xFFFFu);
+  dst[i + half] = uint16_t(pack_bf16x2(y2, 0.0f) & 0xFFFFu);
+}
+
+}  // namespace
+
+void launch_rmsnorm(const float* x, const uint16_t* w, uint16_t* out_bf16, float* out_f32, int rows, int hidden,
+                    float eps, hipStream_t stream) {
+  if (rows == 0) return;
+  rmsnorm_kernel<<<rows, kNormThreads, 0, stream>>>(x, w, out_bf16, out_f32, hidden, eps);
+}
+
+void launch_rope_table(const int32_t* s_pos, float2* cs, int rows, int head_dim, double theta, hipStream_t stream) {
+  const int n = rows * (head_dim / 2);
+  if (n == 0) return;
+  rope_table_kernel<<<(n + 255) / 256, 256, 0, stream>>>(s_pos, cs, rows, head_dim / 2, std::log2(theta));
+}
+
+void launch_rope_split(const float* qkv, const float2* cs, uint16_t* q, uint16_t* k, uint16_t* v, int rows, int hq,
+                       int hkv, int head_dim, hipStream_t stream) {
+  const long n = long(rows) * (hq + 2 * hkv) * (head_dim / 2);
+  if (n == 0) return;
+  rope_split_kernel<<<unsigned((n + 255) / 256), 256, 0, stream>>>(qkv, cs, q, k, v, rows, hq, hkv, head_dim);
+}
+
+}  // namespace epic

@@ -141,3 +141,130 @@ def stage_attention(wl: AttnWorkload, device="cuda", split_blocks: int = 0, spar
 def attention_flops(views: Dict[str, np.ndarray], hq: int, d: int) -> float:
     """Algorithmic attention flops: 4 * Hq * D * sum over S rows of (position + 1)."""
     return 4.0 * hq * d * float(np.sum(views["s_pos"].astype(np.int64) + 1))
+
+
+# ---------------------------------------------------------------- model level
+
+@dataclass
+class ModelStage:
+    wl: object
+    cfg: el.epic_model_cfg
+    weights: List[Dict[str, object]]         # per layer: torch bf16 tensors
+    layers: List[el.epic_layer_weights]
+    final_norm: object
+    k_caches: List[object]                   # per layer: torch bf16 [P, Hkv, 16, D]
+    v_caches: List[object]                   # per layer: torch bf16 [P, Hkv, D, 16]
+    requests: List[el.Request]
+    chunk_block_ids: List[List[int]]
+    sizes: el.epic_plan_sizes
+    views: Dict[str, np.ndarray]
+    dplan: el.DevicePlan
+    emb: object                              # torch fp32 [n_s, hidden]: layer-0 rows of S
+    hidden: object                           # torch fp32 [n_s, hidden], overwritten by a run
+    out: object                              # torch fp32 [n_s, hidden]
+    workspace: object
+
+    def run(self, stream=None):
+        self.hidden.copy_(self.emb)
+        el.epic_link_model(self.cfg, self.layers, self.final_norm, self.dplan, self.hidden, self.k_caches,
+                           self.v_caches, self.out, self.workspace, stream)
+
+
+def model_cfg(wl, n_layers: int) -> el.epic_model_cfg:
+    return el.epic_model_cfg(el.attn_cfg(wl.num_q_heads, wl.num_kv_heads, wl.head_dim), wl.hidden, wl.ffn,
+                             n_layers, wl.rope_theta, wl.rms_eps)
+
+
+def _tok_rows(wl, chunk_ids_of_req, chunk_lens, suffix_len, positions, req=0):
+    """Embeddings of the tokens at the given linked positions of one request."""
+    offs = np.cumsum([0] + list(chunk_lens))
+    out = np.empty((len(positions), wl.hidden), np.float32)
+    for i, p in enumerate(positions):
+        j = int(np.searchsorted(offs, p, side="right") - 1)
+        if j < len(chunk_lens):
+            out[i] = synth.token_embeddings(wl.seed, 0, chunk_ids_of_req[j], [p - offs[j]], wl.hidden)[0]
+        else:
+            out[i] = synth.token_embeddings(wl.seed, 1, req, [p - offs[-1]], wl.hidden)[0]
+    return out
+
+
+def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: float = 0.5, device="cuda",
+                threads: int = 8) -> ModelStage:
+    """Weights, per-chunk caches, link plan and S-row embeddings for a model-level workload.
+
+    caches="compile": every chunk is compiled on the GPU by the library itself (a
+    request with no cached chunks whose suffix is the chunk, positions 0..L-1);
+    caches="synthetic": every layer's chunk caches are seeded N(0, cache_scale^2) draws.
+    """
+    import torch
+
+    L = n_layers or wl.n_layers
+    cfg = model_cfg(wl, L)
+    hq, hkv, d, H = wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.hidden
+    acfg = cfg.attn
+    weights, layers = [], []
+    for layer in range(L):
+        w = synth.model_weights(wl.seed, layer, H, wl.ffn, hq, hkv, d, threads=threads)
+        tw = {k: _bf16_tensor(v, device) for k, v in w.items()}
+        weights.append(tw)
+        layers.append(el.epic_layer_weights(*(tw[k].data_ptr() for k in
+                                              ("attn_norm", "wqkv", "wo", "mlp_norm", "w_gate_up", "w_down"))))
+    final_norm = _bf16_tensor(synth.final_norm_weight(wl.seed, H), device)
+
+    m = len(wl.chunk_lens)
+    nb = [-(-x // el.BLOCK) for x in wl.chunk_lens]
+    link_req0 = el.Request(list(wl.chunk_lens), [[0] * n for n in nb], wl.suffix_len, wl.k)
+    n_priv = el.epic_plan_sizes_get([link_req0], acfg, 1 << 30).n_private
+    num_blocks = sum(nb) + n_priv
+    perm = np.random.default_rng([wl.seed, 99]).permutation(num_blocks).astype(np.int32)
+    chunk_blocks, nxt = [], 0
+    for n in nb:
+        chunk_blocks.append(perm[nxt:nxt + n].tolist())
+        nxt += n
+    free = perm[nxt:]
+    k_caches = [torch.zeros((num_blocks, hkv, el.BLOCK, d), dtype=torch.bfloat16, device=device) for _ in range(L)]
+    v_caches = [torch.zeros((num_blocks, hkv, d, el.BLOCK), dtype=torch.bfloat16, device=device) for _ in range(L)]
+
+    if caches == "compile" and m > 0:
+        # one request per chunk: no cached chunks, the chunk's tokens as new suffix tokens
+        creqs = [el.Request([], [], n_tok, 0) for n_tok in wl.chunk_lens]
+        cfree = [b for blocks in chunk_blocks for b in blocks]
+        csizes, chost, cviews = el.epic_plan_link(creqs, acfg, cfree, num_blocks)
+        assert cviews["priv_block"].tolist() == cfree
+        cplan = el.DevicePlan(csizes, chost, device)
+        emb = np.concatenate([synth.token_embeddings(wl.seed, 0, j, range(n), H)
+                              for j, n in enumerate(wl.chunk_lens)])
+        h = torch.from_numpy(emb).to(device)
+        out = torch.empty_like(h)
+        ws = torch.empty(max(256, el.epic_model_workspace_bytes(cfg, csizes)), dtype=torch.uint8, device=device)
+        el.epic_link_model(cfg, layers, final_norm, cplan, h, k_caches, v_caches, out, ws)
+        torch.cuda.synchronize()
+        del h, out, ws
+    elif caches == "synthetic":
+        for layer in range(L):
+            kp = np.zeros((num_blocks, hkv, el.BLOCK, d), np.uint16)
+            vp = np.zeros((num_blocks, hkv, d, el.BLOCK), np.uint16)
+            for j, n_tok in enumerate(wl.chunk_lens):
+                kr, vr = synth.chunk_cache(wl.seed, j, n_tok, hkv, d, cache_scale, layer=layer)
+                kb, vb = el.pack_blocks(kr, vr)
+                kp[chunk_blocks[j]] = kb
+                vp[chunk_blocks[j]] = vb
+            k_caches[layer] = _bf16_tensor(kp, device)
+            v_caches[layer] = _bf16_tensor(vp, device)
+
+    req = el.Request(list(wl.chunk_lens), chunk_blocks, wl.suffix_len, wl.k)
+    sizes, host, views = el.epic_plan_link([req], acfg, free, num_blocks)
+    dplan = el.DevicePlan(sizes, host, device)
+    emb = _tok_rows(wl, list(range(m)), wl.chunk_lens, wl.suffix_len, views["s_pos"])
+    emb_t = torch.from_numpy(emb).to(device)
+    ws = torch.empty(max(256, el.epic_model_workspace_bytes(cfg, sizes)), dtype=torch.uint8, device=device)
+    return ModelStage(wl=wl, cfg=cfg, weights=weights, layers=layers, final_norm=final_norm, k_caches=k_caches,
+                      v_caches=v_caches, requests=[req], chunk_block_ids=chunk_blocks, sizes=sizes, views=views,
+                      dplan=dplan, emb=emb_t, hidden=torch.empty_like(emb_t), out=torch.empty_like(emb_t),
+                      workspace=ws)
+
+
+def gemm_flops_per_layer(wl, n_rows: int) -> float:
+    """2 * rows * (sum of in * out over the layer's weight matrices)."""
+    qkv = (wl.num_q_heads + 2 * wl.num_kv_heads) * wl.head_dim
+    return 2.0 * n_rows * wl.hidden * (qkv + wl.num_q_heads * wl.head_dim + 3 * wl.ffn)
