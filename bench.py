@@ -40,6 +40,7 @@ WORKLOADS = {
     "c4": ("c4", {}),
     "c2": ("c2", {}),
     "c1": ("c1", {}),
+    "c3": ("c3", {}),
 }
 
 
@@ -112,6 +113,102 @@ def cpu_baseline(st, n_rows: int, seed: int = 1):
     }
 
 
+def cpu_baseline_model(wl, n_rows: int):
+    """Time one decoder layer of the float64 oracle on all S rows (layers run one after
+    another, so the link step is n_layers times this); synthetic caches for that layer."""
+    import numpy as np
+
+    import oracle
+    import synth
+    from threadpoolctl import threadpool_info
+
+    s_pos = oracle.legolink_positions(wl.chunk_lens, wl.suffix_len, wl.k)
+    w = [synth.model_weights(wl.seed, 0, wl.hidden, wl.ffn, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, threads=8)]
+    fn = synth.final_norm_weight(wl.seed, wl.hidden)
+    f = lambda x: synth.bf16_bits_to_f32(x).astype(np.float64)  # noqa: E731
+    ck, cv = [], []
+    for j, L in enumerate(wl.chunk_lens):
+        kb, vb = synth.chunk_cache(wl.seed, j, L, wl.num_kv_heads, wl.head_dim, 0.5, layer=0)
+        ck.append(f(kb))
+        cv.append(f(vb))
+    emb = np.random.default_rng(0).standard_normal((len(s_pos), wl.hidden))
+    t0 = time.perf_counter()
+    oracle.link_model(emb, wl.chunk_lens, wl.suffix_len, wl.k, w, fn, [(ck, cv)], wl.hidden, wl.ffn,
+                      wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.rope_theta, wl.rms_eps)
+    dt = time.perf_counter() - t0
+    cores = max([x.get("num_threads", 1) for x in threadpool_info() if x.get("user_api") == "blas"] or [1])
+    return {
+        "value": round(len(s_pos) / (dt * wl.n_layers), 4),
+        "unit": "recomputed tokens/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"1 of {wl.n_layers} decoder layers on all {len(s_pos)} S rows, float64 NumPy oracle, "
+                   f"{dt:.1f} s; link-step time = {wl.n_layers} x that"),
+        "sample_seconds": round(dt, 2),
+    }
+
+
+def bench_model(args, wl):
+    """Full-model link step (all decoder layers + final norm) on the 32-layer configuration."""
+    import numpy as np
+    import torch
+
+    from paper_2410_15332_amd import epic_link as el
+    from paper_2410_15332_amd import harness
+
+    t0 = time.time()
+    st = harness.stage_model(wl, caches="compile", weights_on_device=True)
+    torch.cuda.synchronize()
+    log(f"staged {wl.name}: n_s={st.sizes.n_s}, {wl.n_layers} layers, chunks compiled on the GPU "
+        f"in {time.time() - t0:.1f}s")
+    for _ in range(args.warmup):
+        st.run()
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for e in (x for row in ev for x in row):
+        e.record()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(K):
+        el.epic_set_profile_events(ev[i])      # records the last layer's attention kernels
+        st.run()
+    end.record()
+    el.epic_set_profile_events(None)
+    torch.cuda.synchronize()
+    step_ms = start.elapsed_time(end) / K
+    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    n_s = st.sizes.n_s
+    attn_flops = harness.attention_flops(st.views, wl.num_q_heads, wl.head_dim)
+    gemm_flops = harness.gemm_flops_per_layer(wl, n_s)
+    total = wl.n_layers * (attn_flops + gemm_flops)
+    achieved = total / (step_ms * 1e-3) / 1e12
+    log(f"step {step_ms:.3f} ms; layer attention {attn_ms:.4f} ms ({attn_flops / attn_ms / 1e9:.1f} TFLOP/s); "
+        f"all layers {achieved:.1f} TFLOP/s")
+    result = {
+        "metric": METRIC, "value": round(n_s / (step_ms * 1e-3), 1), "unit": "recomputed tokens/s", "n_gpus": 1,
+        "steps": K, "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (random-init weights, seeded N(0,1) token embeddings, chunk caches compiled on the GPU)",
+        "config": {"workload": wl.name, "layers": wl.n_layers, "hidden": wl.hidden, "ffn": wl.ffn,
+                   "num_q_heads": wl.num_q_heads, "num_kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim,
+                   "chunks": len(wl.chunk_lens), "chunk_len": wl.chunk_lens[0], "suffix_len": wl.suffix_len,
+                   "k": wl.k, "recomputed_rows": n_s, "linked_tokens": int(st.sizes.max_pos),
+                   "parallelism": "single GPU"},
+        "ttft_ms": round(step_ms, 4),
+        "attention_tflops": round(attn_flops / attn_ms / 1e9, 2),
+        "model_tflops": round(achieved, 2),
+        "roofline": {"bound": "mfma", "kernel": "whole link step (GEMMs + attention)", "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "algorithmic_flops_per_launch": total, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on one decoder layer ...")
+        result["cpu_baseline"] = cpu_baseline_model(wl, args.cpu_rows)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,6 +237,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     name, kw = WORKLOADS[args.workload]
     wl = get_config(name, **kw)
+    if name == "c3":
+        bench_model(args, wl)
+        return
     t0 = time.time()
     st = harness.stage_attention(wl, device="cuda", split_blocks=args.split_blocks)
     torch.cuda.synchronize()

@@ -406,11 +406,16 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
 }
 
 // Merge the split-KV partials of a tile: lse = log2 sum_i 2^lse_i, out = sum_i 2^(lse_i - lse) O_i.
+// Workgroup = (tile, KV head, quarter of the head dim); thread = (tile row, 16 dims).
+constexpr int kCombineParts = 4;
 template <int D>
 __global__ __launch_bounds__(kThreads) void link_combine_kernel(AttnArgs a) {
+  constexpr int DQ = D / kCombineParts;       // dims per workgroup
+  constexpr int DT = DQ / 2;                  // dims per thread (16 or 8)
   const int hkv = a.hkv;
-  const int g = blockIdx.x % hkv;
-  const int tile = blockIdx.x / hkv;
+  const int dq = blockIdx.x % kCombineParts;
+  const int g = (blockIdx.x / kCombineParts) % hkv;
+  const int tile = blockIdx.x / (kCombineParts * hkv);
   const int p0 = a.tiles[4 * tile + 2];
   const int ns = a.tiles[4 * tile + 3];
   if (p0 < 0) return;
@@ -420,19 +425,20 @@ __global__ __launch_bounds__(kThreads) void link_combine_kernel(AttnArgs a) {
   const int srl = t % R, h = g * a.G + t / R;
   if (srl >= nrows) return;
   const int srow = row0 + srl;
+  const int d0 = dq * DQ + hf * DT;
   float mx = -INFINITY;
   for (int i = 0; i < ns; ++i) mx = fmaxf(mx, a.part_lse[(size_t(p0 + i) * hkv + g) * 128 + t]);
-  float acc[D / 2];
+  float acc[DT];
 #pragma unroll
-  for (int d = 0; d < D / 2; ++d) acc[d] = 0.0f;
+  for (int d = 0; d < DT; ++d) acc[d] = 0.0f;
   float wsum = 0.0f;
   for (int i = 0; i < ns; ++i) {
     const float l = a.part_lse[(size_t(p0 + i) * hkv + g) * 128 + t];
     const float w = fast_exp2(l - mx);
     wsum += w;
-    const float* pp = a.part_o + ((size_t(p0 + i) * hkv + g) * 128 + t) * D + hf * (D / 2);
+    const float* pp = a.part_o + ((size_t(p0 + i) * hkv + g) * 128 + t) * D + d0;
 #pragma unroll
-    for (int d = 0; d < D / 2; d += 4) {
+    for (int d = 0; d < DT; d += 4) {
       const float4 f = *reinterpret_cast<const float4*>(pp + d);
       acc[d + 0] += w * f.x;
       acc[d + 1] += w * f.y;
@@ -441,9 +447,9 @@ __global__ __launch_bounds__(kThreads) void link_combine_kernel(AttnArgs a) {
     }
   }
   const float inv = 1.0f / wsum;
-  uint16_t* op = a.out + (size_t(srow) * a.hq + h) * D + hf * (D / 2);
+  uint16_t* op = a.out + (size_t(srow) * a.hq + h) * D + d0;
 #pragma unroll
-  for (int d = 0; d < D / 2; d += 8) {
+  for (int d = 0; d < DT; d += 8) {
     uint4 u;
     u.x = pack_bf16x2(acc[d + 0] * inv, acc[d + 1] * inv);
     u.y = pack_bf16x2(acc[d + 2] * inv, acc[d + 3] * inv);
@@ -451,7 +457,7 @@ __global__ __launch_bounds__(kThreads) void link_combine_kernel(AttnArgs a) {
     u.w = pack_bf16x2(acc[d + 6] * inv, acc[d + 7] * inv);
     *reinterpret_cast<uint4*>(op + d) = u;
   }
-  if (a.lse && hf == 0) a.lse[size_t(srow) * a.hq + h] = (mx + fast_log2(wsum)) * kLn2;
+  if (a.lse && hf == 0 && dq == 0) a.lse[size_t(srow) * a.hq + h] = (mx + fast_log2(wsum)) * kLn2;
 }
 
 }  // namespace
@@ -467,7 +473,7 @@ void launch_link_attention(const AttnArgs& a, int head_dim, int n_work, hipStrea
 
 void launch_link_combine(const AttnArgs& a, int head_dim, int n_tiles, hipStream_t stream) {
   if (n_tiles == 0) return;
-  const dim3 grid(unsigned(n_tiles) * unsigned(a.hkv));
+  const dim3 grid(unsigned(n_tiles) * unsigned(a.hkv) * kCombineParts);
   if (head_dim == 128)
     link_combine_kernel<128><<<grid, kThreads, 0, stream>>>(a);
   else

@@ -8,9 +8,13 @@
 //   kSwiGLU   : act[M][N/2] = silu(gate) * up, bf16  (W_gate_up; gate rows [0, F), up rows [F, 2F))
 //
 // Tiling: 256 threads = 4 wavefronts, workgroup tile 128 x 128, each wavefront
-// 64 x 64 as 2 x 2 v_mfma_f32_32x32x16_bf16 tiles, K in steps of 32 staged in
-// LDS (rows padded to 80 bytes so the 16 rows one ds_read_b128 pass touches
-// fall in distinct banks), double-buffered through registers.  For kSwiGLU the
+// 64 x 64 as 2 x 2 v_mfma_f32_32x32x16_bf16 tiles, K in steps of 64 staged in
+// LDS (rows padded to 144 bytes so the 16 rows one ds_read_b128 pass touches
+// fall in distinct banks).  Global loads run two K steps ahead through two
+// register stages, so each load has two steps of MFMA work to arrive.  Tiles
+// are ordered so that the M tiles sharing one weight tile are launched together
+// on one XCD (workgroups are dealt round-robin to the 8 XCDs), which then reads
+// that weight tile from HBM once and from its L2 afterwards.  For kSwiGLU the
 // 128 weight rows of a tile are gate/up in 32-row groups (gate j.., up j..,
 // gate j+32.., up j+32..), so each wavefront's two 32-column MFMA tiles hold
 // gate and up of the same 32 outputs in the same registers.
@@ -22,9 +26,10 @@ namespace epic {
 
 namespace {
 
-constexpr int kBM = 128, kBN = 128, kBK = 32;
-constexpr int kLdsRow = kBK + 8;   // elements per LDS row (80 bytes)
+constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kLdsRow = kBK + 8;   // elements per LDS row (144 bytes)
 constexpr int kGemmThreads = 256;
+constexpr int kChunks = kBM * kBK / 8 / kGemmThreads;   // 16-byte chunks per thread per operand (4)
 
 template <int EPI>
 __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
@@ -32,8 +37,12 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(16))) uint16_t lds_b[2][kBN * kLdsRow];
 
   const int m_tiles = (g.M + kBM - 1) / kBM;
-  const int mt = blockIdx.x % m_tiles;       // the M tiles of one weight tile are launched together
-  const int nt = blockIdx.x / m_tiles;
+  const int n_tiles = EPI == kSwiGLU ? g.ffn / 64 : g.N / kBN;
+  const int total = m_tiles * n_tiles;
+  int tile_id = blockIdx.x;
+  if (total % 8 == 0) tile_id = (blockIdx.x % 8) * (total / 8) + blockIdx.x / 8;   // XCD-contiguous ranges
+  const int mt = tile_id % m_tiles;
+  const int nt = tile_id / m_tiles;
   const int m0 = mt * kBM;
   const int tid = threadIdx.x & (kGemmThreads - 1);
   const int lane = tid & 63, wave = tid >> 6;
@@ -50,29 +59,36 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
     }
   };
 
-  // global -> register staging: 128 rows x 32 k = 512 chunks of 16 bytes per operand, 2 per thread
-  const int ld_row = tid >> 2, ld_kc = (tid & 3) * 8;        // rows ld_row and ld_row + 64
-  const uint16_t* a_ptr[2];
-  const uint16_t* b_ptr[2];
+  // global -> register staging: chunk i of a thread = row ld_row + 32 i, 8 k at ld_kc
+  const int ld_row = tid >> 3, ld_kc = (tid & 7) * 8;
+  const uint16_t* a_ptr[kChunks];
+  const uint16_t* b_ptr[kChunks];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int r = ld_row + 64 * i;
+  for (int i = 0; i < kChunks; ++i) {
+    const int r = ld_row + 32 * i;
     a_ptr[i] = g.A + size_t(min(m0 + r, g.M - 1)) * g.K + ld_kc;
     b_ptr[i] = g.W + size_t(wrow(r)) * g.K + ld_kc;
   }
-  uint4 ra[2], rb[2];
-  auto load = [&](int kt) {
+  typedef uint32_t stage_t __attribute__((ext_vector_type(8 * kChunks)));   // A then B chunks
+  stage_t st0, st1;
+  auto load = [&](int kt, stage_t& st) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      ra[i] = *reinterpret_cast<const uint4*>(a_ptr[i] + kt * kBK);
-      rb[i] = *reinterpret_cast<const uint4*>(b_ptr[i] + kt * kBK);
+    for (int i = 0; i < kChunks; ++i) {
+      const uint4 a = *reinterpret_cast<const uint4*>(a_ptr[i] + kt * kBK);
+      const uint4 b = *reinterpret_cast<const uint4*>(b_ptr[i] + kt * kBK);
+      st[4 * i + 0] = a.x; st[4 * i + 1] = a.y; st[4 * i + 2] = a.z; st[4 * i + 3] = a.w;
+      st[4 * kChunks + 4 * i + 0] = b.x; st[4 * kChunks + 4 * i + 1] = b.y;
+      st[4 * kChunks + 4 * i + 2] = b.z; st[4 * kChunks + 4 * i + 3] = b.w;
     }
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf, const stage_t& st) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      *reinterpret_cast<uint4*>(&lds_a[buf][(ld_row + 64 * i) * kLdsRow + ld_kc]) = ra[i];
-      *reinterpret_cast<uint4*>(&lds_b[buf][(ld_row + 64 * i) * kLdsRow + ld_kc]) = rb[i];
+    for (int i = 0; i < kChunks; ++i) {
+      *reinterpret_cast<uint4*>(&lds_a[buf][(ld_row + 32 * i) * kLdsRow + ld_kc]) =
+          make_uint4(st[4 * i + 0], st[4 * i + 1], st[4 * i + 2], st[4 * i + 3]);
+      *reinterpret_cast<uint4*>(&lds_b[buf][(ld_row + 32 * i) * kLdsRow + ld_kc]) =
+          make_uint4(st[4 * kChunks + 4 * i + 0], st[4 * kChunks + 4 * i + 1], st[4 * kChunks + 4 * i + 2],
+                     st[4 * kChunks + 4 * i + 3]);
     }
   };
 
@@ -82,27 +98,42 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
-  const int nk = g.K / kBK;
-  load(0);
-  store(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) load(kt + 1);
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
       bf16x8 af[2], bfr[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        af[i] = *reinterpret_cast<const bf16x8*>(&lds_a[cur][(wm * 64 + i * 32 + col) * kLdsRow + ks * 16 + half * 8]);
-        bfr[i] = *reinterpret_cast<const bf16x8*>(&lds_b[cur][(wn * 64 + i * 32 + col) * kLdsRow + ks * 16 + half * 8]);
+        af[i] = *reinterpret_cast<const bf16x8*>(&lds_a[buf][(wm * 64 + i * 32 + col) * kLdsRow + ks * 16 + half * 8]);
+        bfr[i] = *reinterpret_cast<const bf16x8*>(&lds_b[buf][(wn * 64 + i * 32 + col) * kLdsRow + ks * 16 + half * 8]);
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = mfma_32x32x16(af[i], bfr[j], acc[i][j]);
     }
-    if (kt + 1 < nk) store(cur ^ 1);
+  };
+
+  // Pipeline: LDS buffer kt % 2 holds step kt; registers carry steps kt + 1 and kt + 2.
+  const int nk = g.K / kBK;
+  load(0, st0);
+  store(0, st0);
+  if (nk > 1) load(1, st0);
+  if (nk > 2) load(2, st1);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    compute(0);                                // step kt
+    if (kt + 1 < nk) {
+      store(1, st0);                           // step kt + 1
+      if (kt + 3 < nk) load(kt + 3, st0);
+    }
+    __syncthreads();
+    if (kt + 1 >= nk) break;
+    compute(1);                                // step kt + 1
+    if (kt + 2 < nk) {
+      store(0, st1);                           // step kt + 2
+      if (kt + 4 < nk) load(kt + 4, st1);
+    }
     __syncthreads();
   }
 

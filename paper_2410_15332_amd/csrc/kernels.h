@@ -46,7 +46,7 @@ struct GemmArgs {
   uint16_t* act;       // [M][ffn] bf16 (kSwiGLU)
   int M, N, K, ffn;
 };
-// Requirements: K % 32 == 0; N % 128 == 0 (kStoreF32 / kResidual); ffn % 64 == 0 (kSwiGLU).
+// Requirements: K % 64 == 0; N % 128 == 0 (kStoreF32 / kResidual); ffn % 64 == 0 (kSwiGLU).
 void launch_gemm(const GemmArgs& g, int epi, hipStream_t stream);
 
 void launch_rmsnorm(const float* x, const uint16_t* w, uint16_t* out_bf16, float* out_f32, int rows, int hidden,

@@ -68,7 +68,7 @@ epic_status validate_model(const epic_model_cfg* c) {
     return fail(EPIC_ERR_UNSUPPORTED, "hidden %d must be a positive multiple of 128", c->hidden);
   if (c->ffn <= 0 || c->ffn % 128 != 0)
     return fail(EPIC_ERR_UNSUPPORTED, "ffn %d must be a positive multiple of 128", c->ffn);
-  if (((hq + 2 * hkv) * D) % 128 != 0 || (hq * D) % 32 != 0)
+  if (((hq + 2 * hkv) * D) % 128 != 0 || (hq * D) % 64 != 0)
     return fail(EPIC_ERR_UNSUPPORTED, "(Hq + 2 Hkv) * D must be a multiple of 128");
   EPIC_CHECK_ARG(c->n_layers >= 1, "n_layers %d < 1", c->n_layers);
   EPIC_CHECK_ARG(c->rope_theta > 0.0f && c->rms_eps > 0.0f, "rope_theta and rms_eps must be > 0");

@@ -130,20 +130,22 @@ void make_tiles(const epic_link_request* reqs, int batch, int rows_per_tile, std
 }
 
 // Key blocks per split-KV work item.  Rows are split only as far as needed to
-// give about kTargetItems workgroups (8 per CU of 256 CUs, two resident at a
-// time), halving from "no split"; a split never goes below 32 blocks (512
-// keys).  Fewer splits mean fewer partial results to write and merge.
+// give about kTargetItems workgroups (four per workgroup slot of 256 CUs x 2),
+// halving from "no split"; a split never goes below 64 blocks (1024 keys):
+// every split writes and re-reads a 128-row fp32 partial result, which must
+// stay small next to the attention work of the item.
 int split_blocks(const epic_attn_cfg* cfg, const std::vector<Tile>& tiles) {
   if (cfg->kv_split_blocks > 0) return std::max(kKvTileBlocks, cfg->kv_split_blocks / kKvTileBlocks * kKvTileBlocks);
   constexpr int64_t kTargetItems = 2048;
+  constexpr int kMinSplit = 64;
   int max_nblk = kKvTileBlocks;
   for (const Tile& t : tiles) max_nblk = std::max(max_nblk, t.nblk);
   int split = (max_nblk + kKvTileBlocks - 1) / kKvTileBlocks * kKvTileBlocks;
-  while (split > 32) {
+  while (split > kMinSplit) {
     int64_t items = 0;
     for (const Tile& t : tiles) items += std::max(1, cdiv(t.nblk, split));
     if (items * cfg->num_kv_heads >= kTargetItems) break;
-    split = std::max(32, (split / 2 + kKvTileBlocks - 1) / kKvTileBlocks * kKvTileBlocks);
+    split = std::max(kMinSplit, (split / 2 + kKvTileBlocks - 1) / kKvTileBlocks * kKvTileBlocks);
   }
   return split;
 }

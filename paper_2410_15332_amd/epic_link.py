@@ -30,6 +30,14 @@ class EpicError(RuntimeError):
 def _load():
     if not os.path.exists(_LIB_PATH):
         raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2410_15332_amd.build`")
+    # Device memory and streams come from PyTorch, which ships its own HIP runtime
+    # under the same soname (libamdhip64.so.7).  Load torch first so that this
+    # library binds to the runtime already in the process; the other order would
+    # leave torch on a second runtime that sees no device.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     return C.CDLL(_LIB_PATH)
 
 

@@ -188,13 +188,34 @@ def _tok_rows(wl, chunk_ids_of_req, chunk_lens, suffix_len, positions, req=0):
     return out
 
 
+def _device_weights(wl, layer: int, device):
+    """Random-init weights drawn on the device (seeded torch generator), same shapes and
+    distributions as synth.model_weights; for timing runs, where the values do not matter."""
+    import torch
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(wl.seed * 1000 + layer)
+    hq, hkv, d, H, F = wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.hidden, wl.ffn
+
+    def lin(out_f, in_f):
+        return (torch.randn(out_f, in_f, generator=gen, device=device) * (0.5 / in_f ** 0.5)).to(torch.bfloat16)
+
+    def norm(n):
+        return (1.0 + 0.1 * torch.randn(n, generator=gen, device=device)).to(torch.bfloat16)
+
+    return {"attn_norm": norm(H), "wqkv": lin((hq + 2 * hkv) * d, H), "wo": lin(H, hq * d), "mlp_norm": norm(H),
+            "w_gate_up": lin(2 * F, H), "w_down": lin(H, F)}
+
+
 def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: float = 0.5, device="cuda",
-                threads: int = 8) -> ModelStage:
+                threads: int = 8, weights_on_device: bool = False) -> ModelStage:
     """Weights, per-chunk caches, link plan and S-row embeddings for a model-level workload.
 
     caches="compile": every chunk is compiled on the GPU by the library itself (a
     request with no cached chunks whose suffix is the chunk, positions 0..L-1);
     caches="synthetic": every layer's chunk caches are seeded N(0, cache_scale^2) draws.
+    weights_on_device: draw the weights with a seeded device generator (timing runs)
+    instead of synth.model_weights (parity runs).
     """
     import torch
 
@@ -204,8 +225,11 @@ def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: 
     acfg = cfg.attn
     weights, layers = [], []
     for layer in range(L):
-        w = synth.model_weights(wl.seed, layer, H, wl.ffn, hq, hkv, d, threads=threads)
-        tw = {k: _bf16_tensor(v, device) for k, v in w.items()}
+        if weights_on_device:
+            tw = _device_weights(wl, layer, device)
+        else:
+            w = synth.model_weights(wl.seed, layer, H, wl.ffn, hq, hkv, d, threads=threads)
+            tw = {k: _bf16_tensor(v, device) for k, v in w.items()}
         weights.append(tw)
         layers.append(el.epic_layer_weights(*(tw[k].data_ptr() for k in
                                               ("attn_norm", "wqkv", "wo", "mlp_norm", "w_gate_up", "w_down"))))
