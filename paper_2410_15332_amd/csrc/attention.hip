@@ -17,7 +17,7 @@
 // read the same KV blocks through its L2.
 //
 // Per workgroup: 4 wavefronts x 32 rows.  Per iteration 64 keys (4 blocks) are
-// staged in LDS (double-buffered through registers).  S^T = K Q^T and
+// staged in LDS by direct global->LDS loads (two buffers each for K and V).  S^T = K Q^T and
 // O^T += V^T P^T run on v_mfma_f32_32x32x16_bf16: each lane owns one query row
 // (its MFMA column), so the row max / sum need a single lane swap (l <-> l^32).
 // P is rounded to bf16 for the second product; softmax runs in base 2 with
@@ -34,19 +34,31 @@ namespace {
 constexpr int kKT = 64;    // keys per iteration (4 blocks of 16)
 constexpr int kThreads = 256;
 
-// LDS stage: K as [64 keys][D + 8] (16-byte pad: the 16 rows one ds_read_b128
-// pass reads fall in distinct banks); V as the four blocks' [D][16] slabs
-// copied as they are, each 32-byte row's two 16-byte halves swapped when bit
-// 2 xor bit 3 of the row index is set, so that 16 consecutive rows read at the
-// same half hit distinct banks.
+// LDS stage: K as [64 keys][D] and V as the four blocks' [D][16] slabs, both
+// written by direct global->LDS loads (each wavefront instruction fills 1 KB,
+// lane l at byte 16 l), so instead of padding the 16-byte chunks are permuted
+// within a row: K chunk c of key row r sits at c ^ kswz(r), and the two halves
+// of a V row d are swapped when v_swz(d) is set.  The 16 rows one ds_read_b128
+// pass touches then fall in distinct banks.
 template <int D>
 struct AttnLds {
-  static constexpr int KS = D + 8;
-  uint16_t k[2][kKT * KS];
+  uint16_t k[2][kKT * D];
   uint16_t v[2][4 * D * 16];
 };
 
+template <int D>
+__device__ __forceinline__ int kswz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
 __device__ __forceinline__ int v_swz(int d) { return ((d >> 2) ^ (d >> 3)) & 1; }
+
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 16 bytes per lane from global memory straight into LDS at lds_base + 16 * lane.
+__device__ __forceinline__ void dma16(const uint16_t* src, uint16_t* lds_base) {
+  __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)lds_base, 16, 0, 0);
+}
+// wait until this wavefront's outstanding global loads (hence its LDS DMA) are done
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // S^T row rho (0..31 inside a 32-key subtile) holds key (rho>>4)*16 + ((rho>>2)&1)*8 + ((rho>>3)&1)*4 + (rho&3).
 // With this order a lane's accumulator registers 8*st .. 8*st+7 hold the 8
@@ -70,8 +82,6 @@ template <int D>
 __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a) {
   constexpr int NDS = D / 16;                 // k-steps of S^T = K Q^T
   constexpr int NDT = D / 32;                 // 32-row tiles of O^T
-  constexpr int CH = kKT * D / 8 / kThreads;  // 16-byte chunks per thread per operand
-  constexpr int KS = AttnLds<D>::KS;
   __shared__ __attribute__((aligned(16))) AttnLds<D> lds;
 
   const int hkv = a.hkv;
@@ -113,83 +123,58 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   const size_t head_k = size_t(hkv) * 16 * D;   // elements per block (all heads)
   const uint16_t* kbase = a.k_cache + size_t(g) * 16 * D;
   const uint16_t* vbase = a.v_cache + size_t(g) * 16 * D;
-  // staging registers as SSA vectors (an array here ends up in scratch memory):
-  // kreg holds K of a tile two ahead, vreg V of the next tile
-  typedef uint32_t stage_t __attribute__((ext_vector_type(4 * CH)));
-  stage_t kreg, vreg;
+  // Wavefront w stages block w of each KV tile: its 16 K rows (D/32 instructions
+  // of 1 KB) and its [D][16] V slab (D/32 instructions).
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  constexpr int NI = D / 32;                  // 1 KB instructions per operand per wavefront
+  constexpr int KRI = 1024 / (2 * D);         // K rows per instruction (4 or 8)
+  const int k_rl = lane / (D / 8);            // row within an instruction
+  const int k_p = lane % (D / 8);             // chunk position written by this lane
+  const int v_d = lane >> 1, v_p = lane & 1;  // V row within an instruction, half position
 
-  // Chunk i of a thread: K key kkey0 + i*KPT (block (kkey0 + i*KPT) / 16,
-  // compile-time for D = 128), 8 dims at kdc; V block vbeta0 + i*VPB, dim vd,
-  // 8-slot half vhf.
-  constexpr int KPT = kThreads / (D / 8);       // keys covered by one chunk index (16 or 32)
-  constexpr int VPB = kThreads / (2 * D);       // V blocks covered by one chunk index (1 or 2)
-  const int kkey0 = tid / (D / 8), kdc = tid % (D / 8);
-  const int vbeta0 = tid / (2 * D), vd = (tid % (2 * D)) >> 1, vhf = tid & 1;
-
-  // Physical ids of the 4 blocks of KV tile `it` (uniform scalar loads; blocks
-  // past b1 repeat block b1-1, whose keys are masked).
-  auto tile_phys = [&](int it, int (&ph)[4]) {
-    const int bb = b0 + it * 4;
-#pragma unroll
-    for (int beta = 0; beta < 4; ++beta) ph[beta] = lblk[min(bb + beta, b1 - 1)];
+  auto tile_block = [&](int it) {             // physical id of this wavefront's block of tile it
+    return lblk[min(b0 + it * 4 + wv, b1 - 1)];
   };
-  // Global -> registers: K of tile `it` (block ids ph).
-  auto load_k = [&](const int (&ph)[4]) {
+  auto dma_k = [&](int buf, int phys) {
+    const uint16_t* src = kbase + size_t(phys) * head_k;
 #pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int key = kkey0 + i * KPT;
-      int pb;
-      if constexpr (KPT == 16) pb = ph[i];
-      else pb = (key >> 4) == 2 * i ? ph[2 * i] : ph[2 * i + 1];
-      const uint4 x = *reinterpret_cast<const uint4*>(kbase + size_t(pb) * head_k + (key & 15) * D + kdc * 8);
-      kreg[4 * i + 0] = x.x;
-      kreg[4 * i + 1] = x.y;
-      kreg[4 * i + 2] = x.z;
-      kreg[4 * i + 3] = x.w;
+    for (int i = 0; i < NI; ++i) {
+      const int r = KRI * i + k_rl;           // slot (row) inside the block
+      dma16(src + r * D + ((k_p ^ kswz<D>(r)) * 8), &lds.k[buf][(16 * wv + KRI * i) * D]);
     }
   };
-  // Global -> registers: V of tile `it`.  A masked tile zeroes V slots past each
-  // block's end, so stale or NaN bits there never meet a zero softmax weight.
-  auto load_v = [&](int it, const int (&ph)[4]) {
-    const bool fast = it < n_fast;
-    int len[4] = {16, 16, 16, 16};
-    if (!fast) {
-      const int bb = b0 + it * 4;
+  auto dma_v = [&](int buf, int phys) {
+    const uint16_t* src = vbase + size_t(phys) * head_k;
 #pragma unroll
-      for (int beta = 0; beta < 4; ++beta) len[beta] = bb + beta < b1 ? blenp[min(bb + beta, b1 - 1)] : 0;
+    for (int i = 0; i < NI; ++i) {
+      const int d = 32 * i + v_d;
+      dma16(src + d * 16 + ((v_p ^ v_swz(d)) * 8), &lds.v[buf][(wv * D + 32 * i) * 16]);
     }
+  };
+  // After this wavefront's V DMA of tile `it` landed: zero the slots past its
+  // block's end (partial or absent block), so stale or NaN bits never meet a
+  // zero softmax weight.  Tiles in the unmasked prefix need nothing.
+  auto fix_v = [&](int buf, int it) {
+    if (it < n_fast) return;
+    const int blk = b0 + it * 4 + wv;
+    const int len = blk < b1 ? blenp[blk] : 0;
+    if (len >= 16) return;
 #pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      int pb, ln;
-      if constexpr (VPB == 1) {
-        pb = ph[i];
-        ln = len[i];
-      } else {
-        pb = vbeta0 == 0 ? ph[2 * i] : ph[2 * i + 1];
-        ln = vbeta0 == 0 ? len[2 * i] : len[2 * i + 1];
-      }
-      uint4 x = *reinterpret_cast<const uint4*>(vbase + size_t(pb) * head_k + vd * 16 + vhf * 8);
-      if (!fast) {
-        const int valid = ln - vhf * 8;          // valid slots in this 8-slot half
+    for (int i = 0; i < D / 64; ++i) {
+      const int d = lane + 64 * i;
+      uint16_t* row = &lds.v[buf][(wv * D + d) * 16];
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        uint4* q = reinterpret_cast<uint4*>(row + (hf ^ v_swz(d)) * 8);
+        uint4 x = *q;
+        const int valid = len - hf * 8;
         x.x = valid <= 0 ? 0u : valid == 1 ? (x.x & 0xFFFFu) : x.x;
         x.y = valid <= 2 ? 0u : valid == 3 ? (x.y & 0xFFFFu) : x.y;
         x.z = valid <= 4 ? 0u : valid == 5 ? (x.z & 0xFFFFu) : x.z;
         x.w = valid <= 6 ? 0u : valid == 7 ? (x.w & 0xFFFFu) : x.w;
+        *q = x;
       }
-      vreg[4 * i + 0] = x.x;
-      vreg[4 * i + 1] = x.y;
-      vreg[4 * i + 2] = x.z;
-      vreg[4 * i + 3] = x.w;
     }
-  };
-  auto store_k_chunk = [&](int buf, int i) {
-    *reinterpret_cast<uint4*>(&lds.k[buf][(kkey0 + i * KPT) * KS + kdc * 8]) =
-        make_uint4(kreg[4 * i + 0], kreg[4 * i + 1], kreg[4 * i + 2], kreg[4 * i + 3]);
-  };
-  auto store_v_chunk = [&](int buf, int i) {
-    const int beta = vbeta0 + i * VPB;
-    *reinterpret_cast<uint4*>(&lds.v[buf][(beta * D + vd) * 16 + (vhf ^ v_swz(vd)) * 8]) =
-        make_uint4(vreg[4 * i + 0], vreg[4 * i + 1], vreg[4 * i + 2], vreg[4 * i + 3]);
   };
 
   f32x16 o[NDT];
@@ -206,14 +191,18 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   const int krow = srow_key(col);              // K row this lane feeds into S^T
 
   // S^T (64 keys x 32 rows per wave) = K Q^T from LDS stage `buf`; the two
-  // 32-key subtiles alternate so that consecutive MFMAs are independent.
-  const uint16_t* kp_lane = &lds.k[0][krow * KS + half * 8];
+  // 32-key subtiles alternate so that consecutive MFMAs are independent.  The
+  // lane reads key row krow (+32 ks), logical chunk 2s + half (dims 16s + 8 half ..).
+  const uint16_t* kp_lane = &lds.k[0][krow * D];
+  int koff[NDS];
+#pragma unroll
+  for (int s = 0; s < NDS; ++s) koff[s] = ((2 * s + half) ^ kswz<D>(krow)) * 8;
   auto qk = [&](int buf, f32x16 (&sc)[2]) {
-    const uint16_t* kp = kp_lane + buf * (kKT * KS);
+    const uint16_t* kp = kp_lane + buf * (kKT * D);
 #pragma unroll
     for (int q = 0; q < 2 * NDS; ++q) {
       const int ks = q & 1, s = q >> 1;
-      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kp + ks * 32 * KS + s * 16);
+      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kp + ks * 32 * D + koff[s]);
       sc[ks] = mfma_32x32x16(kf, qreg[s], s == 0 ? f32x16{} : sc[ks]);
     }
   };
@@ -222,38 +211,31 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
 
   // Software pipeline over KV tiles.  K runs one tile ahead of V: during
   // iteration it the waves read K(it + 1) (buffer (it + 1) % 2, for S(it + 1))
-  // and V(it) (buffer it % 2), and store K(it + 2) into K buffer it % 2 and
-  // V(it + 1) into V buffer (it + 1) % 2 -- buffers nobody reads in iteration
-  // it, because their last readers ran before the barrier ending iteration
-  // it - 1.  One barrier per iteration; the stores overlap the PV MFMAs.  The
-  // MFMAs of S(it + 1) are interleaved with the exponentials of tile it.
-  int phk[4], phv[4];
-  tile_phys(0, phk);
-  load_k(phk);
-#pragma unroll
-  for (int i = 0; i < CH; ++i) store_k_chunk(0, i);
-  load_v(0, phk);
-#pragma unroll
-  for (int i = 0; i < CH; ++i) store_v_chunk(0, i);
-  if (nkv > 1) {
-    tile_phys(1, phk);
-    load_k(phk);
-#pragma unroll
-    for (int i = 0; i < CH; ++i) store_k_chunk(1, i);
-    load_v(1, phk);                            // V(1): stored during iteration 0
+  // and V(it) (buffer it % 2), while the DMA fills K buffer it % 2 with K(it + 2)
+  // and V buffer (it + 1) % 2 with V(it + 1) -- buffers nobody reads in
+  // iteration it, because their last readers ran before the barrier ending
+  // iteration it - 1.  Each wavefront waits for its own DMA before that
+  // barrier.  The MFMAs of S(it + 1) are interleaved with the exponentials of
+  // tile it.
+  {
+    const int p0 = tile_block(0);
+    dma_k(0, p0);
+    dma_v(0, p0);
+    if (nkv > 1) dma_k(1, tile_block(1));
+    wait_vmem();
+    fix_v(0, 0);
   }
-  tile_phys(2, phk);
-  tile_phys(2, phv);
-  if (nkv > 2) load_k(phk);                    // K(2): stored during iteration 0
-  tile_phys(3, phk);
   __syncthreads();
 
-  f32x16 sacc[2];
-  qk(0, sacc);
+  f32x16 sa[2], sb[2];                         // scores of the current / next tile
+  qk(0, sa);
   __syncthreads();                             // K buffer 0 is rewritten in iteration 0
 
-  for (int it = 0; it < nkv; ++it) {
+  // One KV tile.  sacc holds S(it) on entry; snext receives S(it + 1).
+  auto iteration = [&](const int it, f32x16 (&sacc)[2], f32x16 (&snext)[2]) {
     const int cur = it & 1;
+    if (it + 2 < nkv) dma_k(cur, tile_block(it + 2));
+    if (it + 1 < nkv) dma_v(cur ^ 1, tile_block(it + 1));
 
     // Mask: only tiles past the item's unmasked prefix (diagonal, partial blocks).
     // Register r = i*4 + j of subtile ks holds key ks*32 + (i>>1)*16 + half*8 + (i&1)*4 + j.
@@ -278,14 +260,17 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
         }
     }
 
-    // row max: independent partial maxima, then one lane swap across halves
-    float mx[8];
+    // row max: four chains of three-input maxima, then one lane swap across halves
+    float mx[4];
 #pragma unroll
-    for (int c = 0; c < 8; ++c)
-      mx[c] = fmaxf(fmaxf(sacc[c >> 2][(c & 3) * 4 + 0], sacc[c >> 2][(c & 3) * 4 + 1]),
-                    fmaxf(sacc[c >> 2][(c & 3) * 4 + 2], sacc[c >> 2][(c & 3) * 4 + 3]));
-    const float mt = xhalf_max(fmaxf(fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3])),
-                                     fmaxf(fmaxf(mx[4], mx[5]), fmaxf(mx[6], mx[7]))));
+    for (int c = 0; c < 4; ++c) {
+      const int ks = c >> 1, r0 = (c & 1) * 8;
+      float v = fmaxf(sacc[ks][r0], sacc[ks][r0 + 1]);
+#pragma unroll
+      for (int r = r0 + 2; r < r0 + 8; r += 2) v = fmaxf(fmaxf(v, sacc[ks][r]), sacc[ks][r + 1]);
+      mx[c] = v;
+    }
+    const float mt = xhalf_max(fmaxf(fmaxf(fmaxf(mx[0], mx[1]), mx[2]), mx[3]));
     const float m_cand = fmaxf(m, mt * sl2);
     const bool grow = m_cand > m + kLag;       // also true on the first finite max
     if (__ballot(grow)) {
@@ -300,9 +285,8 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
     const float m_use = m == -INFINITY ? 0.0f : m;
 
     // Exponentials of tile it, interleaved with the S(it + 1) MFMAs.
-    f32x16 snext[2];
     uint32_t pw[16];                           // P(it) packed to bf16 pairs
-    float ps[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    float ps[4];
     auto softmax_step = [&](int q) {
       constexpr int VPS = 32 / (2 * NDS);      // scores per MFMA step
 #pragma unroll
@@ -310,19 +294,19 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
         const int idx = q * VPS + v;           // flattened register (ks = idx / 16, r = idx % 16)
         const float p = fast_exp2(__builtin_fmaf(sacc[idx >> 4][idx & 15], sl2, -m_use));
         sacc[idx >> 4][idx & 15] = p;
-        ps[idx & 3] += p;
+        ps[idx & 3] = idx < 4 ? p : ps[idx & 3] + p;
         if (idx & 1) pw[idx >> 1] = pack_bf16x2(sacc[idx >> 4][(idx & 15) - 1], p);
       }
     };
     if (it + 1 < nkv) {
-      const uint16_t* kp = kp_lane + (cur ^ 1) * (kKT * KS);
+      const uint16_t* kp = kp_lane + (cur ^ 1) * (kKT * D);
       bf16x8 kf[2];                            // K fragments, read one step ahead
-      kf[0] = *reinterpret_cast<const bf16x8*>(kp);
+      kf[0] = *reinterpret_cast<const bf16x8*>(kp + koff[0]);
 #pragma unroll
       for (int q = 0; q < 2 * NDS; ++q) {
         const int ks = q & 1, s = q >> 1;
         if (q + 1 < 2 * NDS)
-          kf[(q + 1) & 1] = *reinterpret_cast<const bf16x8*>(kp + ((q + 1) & 1) * 32 * KS + ((q + 1) >> 1) * 16);
+          kf[(q + 1) & 1] = *reinterpret_cast<const bf16x8*>(kp + ((q + 1) & 1) * 32 * D + koff[(q + 1) >> 1]);
         snext[ks] = mfma_32x32x16(kf[q & 1], qreg[s], s == 0 ? f32x16{} : snext[ks]);
         softmax_step(q);
         __builtin_amdgcn_sched_barrier(0);
@@ -337,7 +321,6 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
     // keys ks*32 + st*16 + half*8 + [0, 8) = packed words 8ks + 4st .. +3; the
     // V^T operand is one 16-byte LDS read; the D/32 accumulators alternate.
     const uint16_t* vp = vp_lane + cur * (4 * D * 16);
-    const bool st_k = it + 2 < nkv, st_v = it + 1 < nkv;
     bf16x8 vf[2];                              // V^T fragments, read one MFMA ahead
     vf[0] = *reinterpret_cast<const bf16x8*>(vp);
 #pragma unroll
@@ -350,29 +333,19 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
         if (n < 4 * NDT)
           vf[n & 1] = *reinterpret_cast<const bf16x8*>(vp + (n / NDT) * D * 16 + (n % NDT) * 32 * 16);
         o[dt] = mfma_32x32x16(vf[(n - 1) & 1], pbk, o[dt]);
-        // LDS stores of K(it + 2) and V(it + 1), spread over the PV MFMAs
-        const int c = n - 1;
-        if (c < CH) {
-          if (st_k) store_k_chunk(cur, c);
-        } else if (c < 2 * CH) {
-          if (st_v) store_v_chunk(cur ^ 1, c - CH);
-        }
-        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    // next global loads: K(it + 3), V(it + 2)
-    if (it + 3 < nkv) load_k(phk);
-    tile_phys(it + 4, phk);
-    if (it + 2 < nkv) {
-      tile_phys(it + 2, phv);
-      load_v(it + 2, phv);
-    }
-
     if (it + 1 < nkv) {
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) sacc[ks] = snext[ks];
-      __syncthreads();                         // stores of this iteration visible; buffers free
+      wait_vmem();                             // this wavefront's DMA of K(it + 2), V(it + 1) landed
+      fix_v(cur ^ 1, it + 1);
+      __syncthreads();                         // ... and everybody's: visible, buffers free
     }
+  };
+
+  // two tiles per trip, so the score buffers swap roles without copies
+  for (int it = 0; it < nkv; it += 2) {
+    iteration(it, sa, sb);
+    if (it + 1 < nkv) iteration(it + 1, sb, sa);
   }
 
   const float ltot = xhalf_sum(lsum);
