@@ -132,9 +132,30 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   const int k_p = lane % (D / 8);             // chunk position written by this lane
   const int v_d = lane >> 1, v_p = lane & 1;  // V row within an instruction, half position
 
-  auto tile_block = [&](int it) {             // physical id of this wavefront's block of tile it
-    return lblk[min(b0 + it * 4 + wv, b1 - 1)];
+  // Block metadata of iteration t, gathered one iteration ahead into lanes of
+  // one register (a vector load that lands with that iteration's DMA, so the
+  // loop never waits on it separately):
+  //   lanes  0..3 : physical ids of tile t + 2 (K DMA in iteration t)
+  //   lanes  4..7 : physical ids of tile t + 1 (V DMA in iteration t)
+  //   lanes  8..11: first positions of tile t's blocks (mask of tile t)
+  //   lanes 12..15: valid slots of tile t's blocks, 0 past b1 (mask of tile t)
+  //   lanes 16..19: valid slots of tile t + 1's blocks (V fix-up in iteration t)
+  auto load_meta = [&](int t) -> int {
+    const int j = lane & 31;
+    int tile_i, kind;
+    if (j < 4) { tile_i = t + 2; kind = 0; }
+    else if (j < 8) { tile_i = t + 1; kind = 0; }
+    else if (j < 12) { tile_i = t; kind = 1; }
+    else if (j < 16) { tile_i = t; kind = 2; }
+    else { tile_i = t + 1; kind = 2; }
+    const int blk = b0 + tile_i * 4 + (j & 3);
+    const int cb = max(b0, min(blk, b1 - 1));    // tile -1 (prologue) and tiles past b1 stay in range
+    const int32_t* arr = kind == 0 ? lblk : kind == 1 ? bpos : blenp;
+    const int x = arr[cb];
+    return (kind == 2 && blk >= b1) ? 0 : x;
   };
+  auto meta_at = [&](int meta, int k) -> int { return __builtin_amdgcn_readlane(meta, k); };
+
   auto dma_k = [&](int buf, int phys) {
     const uint16_t* src = kbase + size_t(phys) * head_k;
 #pragma unroll
@@ -154,11 +175,8 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   // After this wavefront's V DMA of tile `it` landed: zero the slots past its
   // block's end (partial or absent block), so stale or NaN bits never meet a
   // zero softmax weight.  Tiles in the unmasked prefix need nothing.
-  auto fix_v = [&](int buf, int it) {
-    if (it < n_fast) return;
-    const int blk = b0 + it * 4 + wv;
-    const int len = blk < b1 ? blenp[blk] : 0;
-    if (len >= 16) return;
+  auto fix_v = [&](int buf, int it, int len) {
+    if (it < n_fast || len >= 16) return;
 #pragma unroll
     for (int i = 0; i < D / 64; ++i) {
       const int d = lane + 64 * i;
@@ -217,13 +235,17 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   // iteration it - 1.  Each wavefront waits for its own DMA before that
   // barrier.  The MFMAs of S(it + 1) are interleaved with the exponentials of
   // tile it.
+  int meta;                                    // metadata of the current iteration
   {
-    const int p0 = tile_block(0);
+    const int pro = load_meta(-1);               // lanes 0..3: tile 1; 4..7: tile 0; 16..19: lengths of tile 0
+    meta = load_meta(0);
+    wait_vmem();
+    const int p0 = meta_at(pro, 4 + wv);
     dma_k(0, p0);
     dma_v(0, p0);
-    if (nkv > 1) dma_k(1, tile_block(1));
+    if (nkv > 1) dma_k(1, meta_at(pro, wv));
     wait_vmem();
-    fix_v(0, 0);
+    fix_v(0, 0, meta_at(pro, 16 + wv));
   }
   __syncthreads();
 
@@ -234,19 +256,18 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   // One KV tile.  sacc holds S(it) on entry; snext receives S(it + 1).
   auto iteration = [&](const int it, f32x16 (&sacc)[2], f32x16 (&snext)[2]) {
     const int cur = it & 1;
-    if (it + 2 < nkv) dma_k(cur, tile_block(it + 2));
-    if (it + 1 < nkv) dma_v(cur ^ 1, tile_block(it + 1));
+    if (it + 2 < nkv) dma_k(cur, meta_at(meta, wv));
+    if (it + 1 < nkv) dma_v(cur ^ 1, meta_at(meta, 4 + wv));
+    const int meta_next = load_meta(it + 1);   // lands with this iteration's DMA
 
     // Mask: only tiles past the item's unmasked prefix (diagonal, partial blocks).
     // Register r = i*4 + j of subtile ks holds key ks*32 + (i>>1)*16 + half*8 + (i&1)*4 + j.
     if (it >= n_fast) {
-      const int bb = b0 + it * 4;
       int bpos0[4], blen[4];
 #pragma unroll
       for (int beta = 0; beta < 4; ++beta) {
-        const int blk = min(bb + beta, b1 - 1);
-        bpos0[beta] = bpos[blk];
-        blen[beta] = bb + beta < b1 ? blenp[blk] : 0;
+        bpos0[beta] = meta_at(meta, 8 + beta);
+        blen[beta] = meta_at(meta, 12 + beta);
       }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
@@ -337,9 +358,10 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
     }
     if (it + 1 < nkv) {
       wait_vmem();                             // this wavefront's DMA of K(it + 2), V(it + 1) landed
-      fix_v(cur ^ 1, it + 1);
+      fix_v(cur ^ 1, it + 1, meta_at(meta, 16 + wv));
       __syncthreads();                         // ... and everybody's: visible, buffers free
     }
+    meta = meta_next;
   };
 
   // two tiles per trip, so the score buffers swap roles without copies
