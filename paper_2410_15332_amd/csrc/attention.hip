@@ -321,14 +321,18 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
     };
     if (it + 1 < nkv) {
       const uint16_t* kp = kp_lane + (cur ^ 1) * (kKT * D);
-      bf16x8 kf[2];                            // K fragments, read one step ahead
-      kf[0] = *reinterpret_cast<const bf16x8*>(kp + koff[0]);
+      constexpr int NQ = 2 * NDS;
+      bf16x8 kf[3];                            // K fragments, read two steps ahead
+      auto kfrag = [&](int q) {
+        return *reinterpret_cast<const bf16x8*>(kp + (q & 1) * 32 * D + koff[q >> 1]);
+      };
+      kf[0] = kfrag(0);
+      kf[1] = kfrag(1);
 #pragma unroll
-      for (int q = 0; q < 2 * NDS; ++q) {
+      for (int q = 0; q < NQ; ++q) {
         const int ks = q & 1, s = q >> 1;
-        if (q + 1 < 2 * NDS)
-          kf[(q + 1) & 1] = *reinterpret_cast<const bf16x8*>(kp + ((q + 1) & 1) * 32 * D + koff[(q + 1) >> 1]);
-        snext[ks] = mfma_32x32x16(kf[q & 1], qreg[s], s == 0 ? f32x16{} : snext[ks]);
+        if (q + 2 < NQ) kf[(q + 2) % 3] = kfrag(q + 2);
+        snext[ks] = mfma_32x32x16(kf[q % 3], qreg[s], s == 0 ? f32x16{} : snext[ks]);
         softmax_step(q);
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -342,19 +346,21 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
     // keys ks*32 + st*16 + half*8 + [0, 8) = packed words 8ks + 4st .. +3; the
     // V^T operand is one 16-byte LDS read; the D/32 accumulators alternate.
     const uint16_t* vp = vp_lane + cur * (4 * D * 16);
-    bf16x8 vf[2];                              // V^T fragments, read one MFMA ahead
-    vf[0] = *reinterpret_cast<const bf16x8*>(vp);
+    constexpr int NV = 4 * NDT;                // PV MFMAs
+    bf16x8 vf[3];                              // V^T fragments, read two MFMAs ahead
+    auto vfrag = [&](int n) {
+      return *reinterpret_cast<const bf16x8*>(vp + (n / NDT) * D * 16 + (n % NDT) * 32 * 16);
+    };
+    vf[0] = vfrag(0);
+    vf[1] = vfrag(1);
 #pragma unroll
-    for (int kst = 0; kst < 4; ++kst) {
+    for (int n = 0; n < NV; ++n) {
+      const int kst = n / NDT, dt = n % NDT;
+      if (n + 2 < NV) vf[(n + 2) % 3] = vfrag(n + 2);
       const bf16x8 pbk = __builtin_bit_cast(
           bf16x8, make_uint4(pw[4 * kst + 0], pw[4 * kst + 1], pw[4 * kst + 2], pw[4 * kst + 3]));
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) {
-        const int n = kst * NDT + dt + 1;      // next fragment
-        if (n < 4 * NDT)
-          vf[n & 1] = *reinterpret_cast<const bf16x8*>(vp + (n / NDT) * D * 16 + (n % NDT) * 32 * 16);
-        o[dt] = mfma_32x32x16(vf[(n - 1) & 1], pbk, o[dt]);
-      }
+      o[dt] = mfma_32x32x16(vf[n % 3], pbk, o[dt]);
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (it + 1 < nkv) {
       wait_vmem();                             // this wavefront's DMA of K(it + 2), V(it + 1) landed
