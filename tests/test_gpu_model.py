@@ -172,3 +172,20 @@ def test_model_rejects_unsupported_width():
     cfg = el.epic_model_cfg(el.attn_cfg(8, 2, 64), 500, 1024, 1, 5e5, 1e-5)
     s = el.epic_plan_sizes()
     assert el.epic_model_workspace_bytes(cfg, s) == 0
+
+
+def test_recompute_all_wide_output_tiles():
+    """A recompute-all link of 4100 rows at hidden 1024: enough row tiles that every
+    projection (W_O and W_down included) runs on 128-column output tiles, where the
+    short link steps above run their narrow outputs on 64-column tiles."""
+    wl = _small("fr_wide", [2000, 2000], 100, -1, hidden=1024, ffn=2048, hq=8, hkv=2, d=128, layers=1)
+    st = _stage(wl, caches="synthetic")
+    st.run()
+    torch.cuda.synchronize()
+    assert st.sizes.n_s == 4100
+    ws, fn = _oracle_inputs(wl, 1)
+    emb = _s_embeddings(wl, np.arange(4100))
+    full, _ = oracle.compile_chunk(emb, ws, fn, bf16_storage=True, **_dims(wl))
+    err = np.abs(st.out.double().cpu().numpy() - full).max()
+    print(f"[gpu-test] fr_wide: final hidden max|err| {err:.3e}", flush=True)
+    assert err <= ATOL, err
