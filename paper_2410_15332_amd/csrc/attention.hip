@@ -16,13 +16,20 @@
 // planner orders items key-segment first, so concurrent workgroups on an XCD
 // read the same KV blocks through its L2.
 //
-// Per workgroup: 4 wavefronts x 32 rows.  Per iteration 64 keys (4 blocks) are
-// staged in LDS by direct global->LDS loads (two buffers each for K and V).  S^T = K Q^T and
-// O^T += V^T P^T run on v_mfma_f32_32x32x16_bf16: each lane owns one query row
-// (its MFMA column), so the row max / sum need a single lane swap (l <-> l^32).
-// P is rounded to bf16 for the second product; softmax runs in base 2 with
-// scale*log2(e) applied inside the exponent's FMA; the running output is
-// rescaled only when some row's maximum grew; accumulation is fp32.
+// Per workgroup: 4 wavefronts x 32 rows.  Per step 64 keys (4 blocks) are
+// staged in LDS by direct buffer->LDS loads (two buffers each for K and V).
+// S^T = K Q^T and O^T += V^T P^T run on v_mfma_f32_32x32x16_bf16: each lane
+// owns one query row (its MFMA column), so the row max / sum need a single lane
+// swap (l <-> l^32).  P is rounded to bf16 for the second product; softmax runs
+// in base 2 with scale*log2(e) applied inside the exponent's FMA; the running
+// output is rescaled only when some row's maximum grew; accumulation is fp32.
+//
+// Software pipeline: step i issues the PV product of tile i-1 and the QK
+// product of tile i+1, alternating, and spreads the softmax of tile i (row
+// maximum, then the 32 exponentials per lane) over those 32 MFMAs, so the
+// matrix cores always have independent work beside the vector ALU work.
+#include <utility>
+
 #include "device_common.h"
 #include "kernels.h"
 #include "plan_internal.h"
@@ -31,33 +38,72 @@ namespace epic {
 
 namespace {
 
-constexpr int kKT = 64;    // keys per iteration (4 blocks of 16)
+constexpr int kKT = 64;    // keys per step (4 blocks of 16)
 constexpr int kThreads = 256;
+// Word 3 of a gfx9-family raw buffer descriptor (32-bit data format, no swizzle).
+constexpr int kBufWord3 = 0x00020000;
 
-// LDS stage: K as [64 keys][D] and V as the four blocks' [D][16] slabs, both
-// written by direct global->LDS loads (each wavefront instruction fills 1 KB,
-// lane l at byte 16 l), so instead of padding the 16-byte chunks are permuted
-// within a row: K chunk c of key row r sits at c ^ kswz(r), and the two halves
-// of a V row d are swapped when v_swz(d) is set.  The 16 rows one ds_read_b128
-// pass touches then fall in distinct banks.
+// LDS stage, written by direct buffer->LDS loads (each wavefront instruction
+// fills 1 KB, lane l at byte 16 l):
+//   K as [block][row group g = row / 8][chunk c ^ g][row % 8] in 16-byte units
+//     (c = 16-byte chunk of the head dim) -- each load instruction reads 8 whole
+//     rows of a block; the 16 lanes of one ds_read_b128 group read chunk c of 16
+//     consecutive keys as two 128-byte runs half a bank-row apart (the ^ g),
+//     and every K operand sits at a fixed offset from the lane's base;
+//   V as the four blocks' [D][16] slabs with the two halves of row d swapped
+//     when v_swz(d) is set, so the 16 rows one group touches fall in distinct banks.
+//   Q: the last kQl<D> 16-dim slices of every lane's query row (16 bytes per
+//     lane each), which would not fit in registers beside the rest.
+template <int D>
+constexpr int kQl = D == 128 ? 2 : 0;
 template <int D>
 struct AttnLds {
   uint16_t k[2][kKT * D];
   uint16_t v[2][4 * D * 16];
+  uint16_t q[kQl<D> > 0 ? kQl<D> : 1][kThreads * 8];
 };
 
-template <int D>
-__device__ __forceinline__ int kswz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
 __device__ __forceinline__ int v_swz(int d) { return ((d >> 2) ^ (d >> 3)) & 1; }
 
-typedef __attribute__((address_space(1))) void global_void;
 typedef __attribute__((address_space(3))) void lds_void;
 
-// 16 bytes per lane from global memory straight into LDS at lds_base + 16 * lane.
-__device__ __forceinline__ void dma16(const uint16_t* src, uint16_t* lds_base) {
-  __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)lds_base, 16, 0, 0);
+// One wavefront's share of a block: D/32 loads of 16 bytes per lane from the
+// block's descriptor into LDS.  Load I lands lane l at LDS byte dst + 1024 I + 16 l
+// and reads block byte voff(I) + GOFF(I); the instruction offset GOFF(I) moves
+// both addresses, so the LDS base handed to load I is dst + 1024 I - GOFF(I).
+template <class GOFF, int... I>
+__device__ __forceinline__ void dma_block(__amdgpu_buffer_rsrc_t rs, char* dst, int voff_even, int voff_odd,
+                                          std::integer_sequence<int, I...>) {
+  (__builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + 1024 * I - GOFF::template at<I>()), 16,
+                                            GOFF::template odd<I>() ? voff_odd : voff_even, 0,
+                                            GOFF::template at<I>(), 0),
+   ...);
 }
-// wait until this wavefront's outstanding global loads (hence its LDS DMA) are done
+// K load I of a D-wide block: row group rb = 64 I / (8 NCH), chunk base v0 = (64 I % (8 NCH)) / 8;
+// lane l reads row 8 rb + l % 8, chunk (v0 + l / 8) ^ rb.
+template <int D>
+struct KLoads {
+  static constexpr int NCH = D / 8;
+  template <int I> static constexpr int rb() { return 64 * I / (8 * NCH); }
+  template <int I> static constexpr int at() { return 16 * rb<I>() * D + 16 * ((64 * I % (8 * NCH)) / 8); }
+  template <int I> static constexpr bool odd() { return rb<I>() & 1; }
+};
+// V load I: rows 32 I .. 32 I + 31 of the [D][16] slab, 1 KB contiguous.
+struct VLoads {
+  template <int I> static constexpr int at() { return 1024 * I; }
+  template <int I> static constexpr bool odd() { return false; }
+};
+// f(integral_constant<int, I>) for I = 0 .. N-1, every index a compile-time constant
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// wait until this wavefront's outstanding vector memory loads (hence its LDS DMA) are done
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // S^T row rho (0..31 inside a 32-key subtile) holds key (rho>>4)*16 + ((rho>>2)&1)*8 + ((rho>>3)&1)*4 + (rho&3).
@@ -82,6 +128,8 @@ template <int D>
 __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a) {
   constexpr int NDS = D / 16;                 // k-steps of S^T = K Q^T
   constexpr int NDT = D / 32;                 // 32-row tiles of O^T
+  constexpr int NSLOT = 2 * NDS;              // QK MFMAs per tile (= PV MFMAs, 4 * NDT)
+  static_assert(NSLOT == 4 * NDT, "QK and PV MFMA counts pair up");
   __shared__ __attribute__((aligned(16))) AttnLds<D> lds;
 
   const int hkv = a.hkv;
@@ -95,9 +143,6 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   const int n_fast = wk[4];                    // leading KV tiles that need no mask
   const int row0 = a.tiles[4 * tile + 0];
   const int nrows = a.tiles[4 * tile + 1];
-  const int32_t* __restrict__ lblk = a.linked_blocks;
-  const int32_t* __restrict__ bpos = a.block_pos0;
-  const int32_t* __restrict__ blenp = a.block_len;
 
   const int tid = threadIdx.x & (kThreads - 1);   // blockDim.x == kThreads
   const int lane = tid & 63, wave = tid >> 6;
@@ -109,69 +154,69 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   const int srow = row0 + (row_ok ? srl : nrows - 1);
   const int qpos = a.s_pos[srow];
 
-  bf16x8 qreg[NDS];
+  // Q operand of k-step s (dims 16 s + 8 half ..): registers for s < NQR, LDS above
+  constexpr int NQR = NDS - kQl<D>;
+  bf16x8 qreg[NQR];
   {
     const uint16_t* qp = a.q + (size_t(srow) * a.hq + h) * D + half * 8;
 #pragma unroll
     for (int s = 0; s < NDS; ++s) {
-      qreg[s] = *reinterpret_cast<const bf16x8*>(qp + s * 16);
-      if (!row_ok) qreg[s] = bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      bf16x8 x = *reinterpret_cast<const bf16x8*>(qp + s * 16);
+      if (!row_ok) x = bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      if (s < NQR) qreg[s < NQR ? s : 0] = x;
+      else *reinterpret_cast<bf16x8*>(&lds.q[s - NQR][tid * 8]) = x;
     }
   }
+  auto qfrag = [&](int s) -> bf16x8 {
+    return s < NQR ? qreg[s < NQR ? s : 0] : *reinterpret_cast<const bf16x8*>(&lds.q[s - NQR][tid * 8]);
+  };
 
   const int nkv = (b1 - b0 + 3) / 4;
-  const size_t head_k = size_t(hkv) * 16 * D;   // elements per block (all heads)
-  const uint16_t* kbase = a.k_cache + size_t(g) * 16 * D;
-  const uint16_t* vbase = a.v_cache + size_t(g) * 16 * D;
-  // Wavefront w stages block w of each KV tile: its 16 K rows (D/32 instructions
-  // of 1 KB) and its [D][16] V slab (D/32 instructions).
+  // Wavefront w stages block w of each KV tile: its 16 K rows and its [D][16]
+  // V slab, D/32 loads of 1 KB each, through a descriptor over that block.
   const int wv = __builtin_amdgcn_readfirstlane(wave);
-  constexpr int NI = D / 32;                  // 1 KB instructions per operand per wavefront
-  constexpr int KRI = 1024 / (2 * D);         // K rows per instruction (4 or 8)
-  const int k_rl = lane / (D / 8);            // row within an instruction
-  const int k_p = lane % (D / 8);             // chunk position written by this lane
-  const int v_d = lane >> 1, v_p = lane & 1;  // V row within an instruction, half position
+  constexpr int NI = D / 32;                  // 1 KB loads per operand per wavefront
+  constexpr int NCH = D / 8;                  // 16-byte chunks per K row
+  const char* kbase = reinterpret_cast<const char*>(a.k_cache + size_t(g) * 16 * D);
+  const char* vbase = reinterpret_cast<const char*>(a.v_cache + size_t(g) * 16 * D);
+  const size_t blk_bytes = size_t(hkv) * 16 * D * 2;   // one physical block, all heads
+  // Lane byte offsets in the block, the per-load constant part left to the
+  // instruction offset: K load i reads row 8 rb + l % 8, chunk (v0 + l / 8) ^ rb,
+  // block byte (l % 8) 2D + ((l / 8) ^ rb) 16 + [16 rb D + 16 v0]; V load i reads
+  // row d = 32 i + l / 2, half (l & 1) ^ v_swz(d) = (l & 1) ^ v_swz(l / 2), block
+  // byte 32 (l / 2) + 16 ((l & 1) ^ v_swz(l / 2)) + [1024 i].
+  const int kvo = (lane & 7) * 2 * D + (lane >> 3) * 16;
+  const int vvo = (lane >> 1) * 32 + ((lane & 1) ^ v_swz(lane >> 1)) * 16;
+  auto dma_k = [&](int buf, int phys) {
+    const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(kbase) + size_t(phys) * blk_bytes, 0,
+                                                      16 * D * 2, kBufWord3);
+    dma_block<KLoads<D>>(rs, reinterpret_cast<char*>(&lds.k[buf][16 * wv * D]), kvo, kvo ^ 16,
+                         std::make_integer_sequence<int, NI>{});
+  };
+  auto dma_v = [&](int buf, int phys) {
+    const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(vbase) + size_t(phys) * blk_bytes, 0,
+                                                      16 * D * 2, kBufWord3);
+    dma_block<VLoads>(rs, reinterpret_cast<char*>(&lds.v[buf][wv * D * 16]), vvo, vvo,
+                      std::make_integer_sequence<int, NI>{});
+  };
 
-  // Block metadata of iteration t, gathered one iteration ahead into lanes of
-  // one register (a vector load that lands with that iteration's DMA, so the
-  // loop never waits on it separately):
-  //   lanes  0..3 : physical ids of tile t + 2 (K DMA in iteration t)
-  //   lanes  4..7 : physical ids of tile t + 1 (V DMA in iteration t)
+  // Block metadata of step t, gathered one step ahead into lanes of one
+  // register (a vector load that lands with that step's DMA):
+  //   lanes  0..3 : physical ids of tile t + 2 (K DMA in step t)
+  //   lanes  4..7 : physical ids of tile t     (V DMA in step t)
   //   lanes  8..11: first positions of tile t's blocks (mask of tile t)
-  //   lanes 12..15: valid slots of tile t's blocks, 0 past b1 (mask of tile t)
-  //   lanes 16..19: valid slots of tile t + 1's blocks (V fix-up in iteration t)
-  auto load_meta = [&](int t) -> int {
-    const int j = lane & 31;
-    int tile_i, kind;
-    if (j < 4) { tile_i = t + 2; kind = 0; }
-    else if (j < 8) { tile_i = t + 1; kind = 0; }
-    else if (j < 12) { tile_i = t; kind = 1; }
-    else if (j < 16) { tile_i = t; kind = 2; }
-    else { tile_i = t + 1; kind = 2; }
-    const int blk = b0 + tile_i * 4 + (j & 3);
-    const int cb = max(b0, min(blk, b1 - 1));    // tile -1 (prologue) and tiles past b1 stay in range
-    const int32_t* arr = kind == 0 ? lblk : kind == 1 ? bpos : blenp;
-    const int x = arr[cb];
-    return (kind == 2 && blk >= b1) ? 0 : x;
+  //   lanes 12..15: valid slots of tile t's blocks, 0 past b1 (mask, V fix-up)
+  const int mj = lane & 31;
+  const int m_kind = mj < 8 ? 0 : (mj < 12 ? 1 : 2);
+  const int m_toff = mj < 4 ? 2 : 0;
+  const int32_t* m_arr = m_kind == 0 ? a.linked_blocks : (m_kind == 1 ? a.block_pos0 : a.block_len);
+  auto load_meta = [&](int ts) -> int {
+    const int blk = b0 + 4 * (ts + m_toff) + (mj & 3);
+    const int x = m_arr[max(b0, min(blk, b1 - 1))];   // tiles before 0 / past b1 stay in range
+    return (m_kind == 2 && blk >= b1) ? 0 : x;
   };
   auto meta_at = [&](int meta, int k) -> int { return __builtin_amdgcn_readlane(meta, k); };
 
-  auto dma_k = [&](int buf, int phys) {
-    const uint16_t* src = kbase + size_t(phys) * head_k;
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int r = KRI * i + k_rl;           // slot (row) inside the block
-      dma16(src + r * D + ((k_p ^ kswz<D>(r)) * 8), &lds.k[buf][(16 * wv + KRI * i) * D]);
-    }
-  };
-  auto dma_v = [&](int buf, int phys) {
-    const uint16_t* src = vbase + size_t(phys) * head_k;
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int d = 32 * i + v_d;
-      dma16(src + d * 16 + ((v_p ^ v_swz(d)) * 8), &lds.v[buf][(wv * D + 32 * i) * 16]);
-    }
-  };
   // After this wavefront's V DMA of tile `it` landed: zero the slots past its
   // block's end (partial or absent block), so stale or NaN bits never meet a
   // zero softmax weight.  Tiles in the unmasked prefix need nothing.
@@ -208,57 +253,58 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   const float sl2 = a.scale_log2;
   const int krow = srow_key(col);              // K row this lane feeds into S^T
 
-  // S^T (64 keys x 32 rows per wave) = K Q^T from LDS stage `buf`; the two
-  // 32-key subtiles alternate so that consecutive MFMAs are independent.  The
-  // lane reads key row krow (+32 ks), logical chunk 2s + half (dims 16s + 8 half ..).
-  const uint16_t* kp_lane = &lds.k[0][krow * D];
-  int koff[NDS];
-#pragma unroll
-  for (int s = 0; s < NDS; ++s) koff[s] = ((2 * s + half) ^ kswz<D>(krow)) * 8;
-  auto qk = [&](int buf, f32x16 (&sc)[2]) {
-    const uint16_t* kp = kp_lane + buf * (kKT * D);
-#pragma unroll
-    for (int q = 0; q < 2 * NDS; ++q) {
-      const int ks = q & 1, s = q >> 1;
-      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kp + ks * 32 * D + koff[s]);
-      sc[ks] = mfma_32x32x16(kf, qreg[s], s == 0 ? f32x16{} : sc[ks]);
-    }
-  };
+  // S^T (64 keys x 32 rows per wave) = K Q^T: MFMA q = (subtile q & 1, k-step
+  // q >> 1); the lane reads key krow + 32 subtile (block 2 subtile + krow / 16,
+  // row r = krow % 16, group r / 8), chunk c = 2 s + half, stored at chunk
+  // position c ^ (r / 8) = 2 s + (half ^ (r / 8)).
+  const int kr = krow & 15;
+  const uint16_t* kp_lane =
+      &lds.k[0][((krow >> 4) * 16 * NCH + (kr >> 3) * 8 * NCH + (half ^ (kr >> 3)) * 8 + (kr & 7)) * 8];
   // V^T operand of lane: row d = dt*32 + col, 16-byte half (half ^ swz(col)) of the row.
   const uint16_t* vp_lane = &lds.v[0][col * 16 + (half ^ v_swz(col)) * 8];
+  auto kfrag = [&](int buf, int q) {
+    return *reinterpret_cast<const bf16x8*>(kp_lane + buf * (kKT * D) + (q & 1) * (2 * 16 * NCH * 8) +
+                                            (q >> 1) * (2 * 8 * 8));
+  };
+  // PV MFMA n = (16-key step n / NDT, O^T tile n % NDT)
+  auto vfrag = [&](int buf, int n) {
+    return *reinterpret_cast<const bf16x8*>(vp_lane + buf * (4 * D * 16) + (n / NDT) * D * 16 + (n % NDT) * 32 * 16);
+  };
+  // P of a tile as 4 MFMA B operands: operand kst = keys kst*16 + half*8 + [0, 8)
+  // as bf16 pairs (score registers 8 kst .. 8 kst + 7 of the S^T layout)
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  auto pfrag = [&](const u32x4 (&p)[4], int kst) { return __builtin_bit_cast(bf16x8, p[kst]); };
 
-  // Software pipeline over KV tiles.  K runs one tile ahead of V: during
-  // iteration it the waves read K(it + 1) (buffer (it + 1) % 2, for S(it + 1))
-  // and V(it) (buffer it % 2), while the DMA fills K buffer it % 2 with K(it + 2)
-  // and V buffer (it + 1) % 2 with V(it + 1) -- buffers nobody reads in
-  // iteration it, because their last readers ran before the barrier ending
-  // iteration it - 1.  Each wavefront waits for its own DMA before that
-  // barrier.  The MFMAs of S(it + 1) are interleaved with the exponentials of
-  // tile it.
-  int meta;                                    // metadata of the current iteration
+  int meta = 0;                                // metadata of the current step
   {
-    const int pro = load_meta(-1);               // lanes 0..3: tile 1; 4..7: tile 0; 16..19: lengths of tile 0
-    meta = load_meta(0);
+    const int pro = load_meta(-1);             // lanes 0..3: ids of tile 1
+    meta = load_meta(0);                       // lanes 4..7: ids of tile 0
     wait_vmem();
-    const int p0 = meta_at(pro, 4 + wv);
-    dma_k(0, p0);
-    dma_v(0, p0);
+    dma_k(0, meta_at(meta, 4 + wv));
     if (nkv > 1) dma_k(1, meta_at(pro, wv));
     wait_vmem();
-    fix_v(0, 0, meta_at(pro, 16 + wv));
   }
   __syncthreads();
 
-  f32x16 sa[2], sb[2];                         // scores of the current / next tile
-  qk(0, sa);
-  __syncthreads();                             // K buffer 0 is rewritten in iteration 0
+  f32x16 s0[2], s1[2];                         // scores of even / odd tiles
+  u32x4 p0[4], p1[4];                          // P of even / odd tiles, packed bf16 pairs
+#pragma unroll
+  for (int q = 0; q < NSLOT; ++q) {
+    const int ks = q & 1, s = q >> 1;
+    s0[ks] = mfma_32x32x16(kfrag(0, q), qfrag(s), s == 0 ? f32x16{} : s0[ks]);
+  }
+  __syncthreads();                             // K buffer 0 is rewritten in step 0
 
-  // One KV tile.  sacc holds S(it) on entry; snext receives S(it + 1).
-  auto iteration = [&](const int it, f32x16 (&sacc)[2], f32x16 (&snext)[2]) {
+  // One step over tile it.  sc = S(it) on entry (complete); pp = P(it - 1) (PV
+  // only); the step leaves P(it) in pc and S(it + 1) in sn (QK only).
+  auto step = [&](auto pv_tag, auto qk_tag, const int it, f32x16 (&sc)[2], f32x16 (&sn)[2],
+                  const u32x4 (&pp)[4], u32x4 (&pc)[4]) __attribute__((always_inline)) {
+    constexpr bool PV = decltype(pv_tag)::value;
+    constexpr bool QK = decltype(qk_tag)::value;
     const int cur = it & 1;
-    if (it + 2 < nkv) dma_k(cur, meta_at(meta, wv));
-    if (it + 1 < nkv) dma_v(cur ^ 1, meta_at(meta, 4 + wv));
-    const int meta_next = load_meta(it + 1);   // lands with this iteration's DMA
+    if (it + 2 < nkv) dma_k(cur, meta_at(meta, wv));          // K(it + 2): its buffer held K(it)
+    dma_v(cur, meta_at(meta, 4 + wv));                         // V(it): its buffer held V(it - 2)
+    const int meta_next = load_meta(it + 1);                   // lands with this step's DMA
 
     // Mask: only tiles past the item's unmasked prefix (diagonal, partial blocks).
     // Register r = i*4 + j of subtile ks holds key ks*32 + (i>>1)*16 + half*8 + (i&1)*4 + j.
@@ -277,103 +323,128 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
           const int beta = ks * 2 + (i >> 1);
           const int slot = half * 8 + (i & 1) * 4 + j;
           const bool ok = slot < blen[beta] && bpos0[beta] + slot <= qpos;
-          sacc[ks][r] = ok ? sacc[ks][r] : -INFINITY;
+          sc[ks][r] = ok ? sc[ks][r] : -INFINITY;
         }
     }
 
-    // row max: four chains of three-input maxima, then one lane swap across halves
-    float mx[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int ks = c >> 1, r0 = (c & 1) * 8;
-      float v = fmaxf(sacc[ks][r0], sacc[ks][r0 + 1]);
-#pragma unroll
-      for (int r = r0 + 2; r < r0 + 8; r += 2) v = fmaxf(fmaxf(v, sacc[ks][r]), sacc[ks][r + 1]);
-      mx[c] = v;
+    const int rb = cur ^ 1;                    // buffers read in this step: K(it + 1), V(it - 1)
+    bf16x8 kf[3], vf[3], qf[2];                // operands, read two MFMAs ahead
+    if (PV) { vf[0] = vfrag(rb, 0); vf[1] = vfrag(rb, 1); }
+    if (!PV && QK) {
+      kf[0] = kfrag(rb, 0);
+      kf[1] = kfrag(rb, 1);
     }
-    const float mt = xhalf_max(fmaxf(fmaxf(fmaxf(mx[0], mx[1]), mx[2]), mx[3]));
-    const float m_cand = fmaxf(m, mt * sl2);
-    const bool grow = m_cand > m + kLag;       // also true on the first finite max
-    if (__ballot(grow)) {
-      const float alpha = grow ? fast_exp2(m - m_cand) : 1.0f;
-      m = grow ? m_cand : m;
-      lsum *= alpha;
+
+    float mx[4], m_cand = 0.0f, alpha = 1.0f, m_use = 0.0f;
+    bool grow = false;
+    float ps[4];
+    // MFMA slots: 0 .. NSLOT-1 the PV product of tile it - 1, NSLOT .. 2 NSLOT-1
+    // the QK product of tile it + 1 (so S(it + 1) fills while S(it) drains).
+    // Softmax work of tile it per slot: slots 0..3 the row maximum and the
+    // rescale decision, slots 4.. the exponentials (unit u = score u).
+    constexpr int kMaxSlots = 4;
+    constexpr int NS2 = 2 * NSLOT;
+    auto exp_unit = [&](auto uc) __attribute__((always_inline)) {
+      constexpr int u = decltype(uc)::value;
+      const float p = fast_exp2(__builtin_fmaf(sc[u >> 4][u & 15], sl2, -m_use));
+      sc[u >> 4][u & 15] = p;
+      ps[u & 3] = u < 4 ? p : ps[u & 3] + p;
+      if constexpr (u & 1) {
+        pc[u >> 3][(u >> 1) & 3] = pack_bf16x2(sc[u >> 4][(u & 15) - 1], p);
+        // keep the pair's exponentials in this slot: P is only read in the next
+        // step, and the compiler would otherwise sink them all to that first use
+        __asm__ volatile("" ::"v"(pc[u >> 3][(u >> 1) & 3]));
+      }
+    };
+    static_for<NS2>([&](auto qc) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      if constexpr (q + 2 < NSLOT) {
+        if constexpr (PV) vf[(q + 2) % 3] = vfrag(rb, q + 2);
+      } else if constexpr (q + 2 < NS2) {
+        constexpr int k2 = q + 2 - NSLOT;
+        if constexpr (QK && (PV || k2 >= 2)) {
+          kf[k2 % 3] = kfrag(rb, k2);
+          if constexpr ((k2 & 1) == 0 && (k2 >> 1) >= NQR) qf[((k2 >> 1) - NQR) & 1] = qfrag(k2 >> 1);
+        }
+      }
+      if constexpr (q < NSLOT) {
+        if constexpr (PV) o[q % NDT] = mfma_32x32x16(vf[q % 3], pfrag(pp, q / NDT), o[q % NDT]);
+      } else {
+        constexpr int k = q - NSLOT;
+        if constexpr (QK) {
+          bf16x8 qo;
+          if constexpr ((k >> 1) < NQR) qo = qreg[(k >> 1) < NQR ? (k >> 1) : 0];
+          else qo = qf[((k >> 1) - NQR) & 1];
+          sn[k & 1] = mfma_32x32x16(kf[k % 3], qo, (k >> 1) == 0 ? f32x16{} : sn[k & 1]);
+        }
+      }
+      if constexpr (q == 0) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int ks = c >> 1, r0 = (c & 1) * 8;
+          mx[c] = fmaxf(fmaxf(fmaxf(sc[ks][r0], sc[ks][r0 + 1]), sc[ks][r0 + 2]), sc[ks][r0 + 3]);
+        }
+      } else if constexpr (q == 1) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int ks = c >> 1, r0 = (c & 1) * 8 + 4;
+          mx[c] = fmaxf(fmaxf(fmaxf(mx[c], sc[ks][r0]), sc[ks][r0 + 1]), fmaxf(sc[ks][r0 + 2], sc[ks][r0 + 3]));
+        }
+      } else if constexpr (q == 2) {
+        const float mt = xhalf_max(fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3])));
+        m_cand = fmaxf(m, mt * sl2);
+      } else if constexpr (q == 3) {
+        grow = m_cand > m + kLag;              // also true on the first finite max
+        alpha = grow ? fast_exp2(m - m_cand) : 1.0f;
+        m = grow ? m_cand : m;
+        m_use = m == -INFINITY ? 0.0f : m;
+      } else {
+        static_for<32>([&](auto uc) __attribute__((always_inline)) {
+          if constexpr (kMaxSlots + (decltype(uc)::value * (NS2 - kMaxSlots)) / 32 == q) exp_unit(uc);
+        });
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    lsum = lsum * alpha + ((ps[0] + ps[1]) + (ps[2] + ps[3]));
+    if (PV && __ballot(grow)) {                // O holds PV(it - 1): move it to the new maximum
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
     }
-    const float m_use = m == -INFINITY ? 0.0f : m;
-
-    // Exponentials of tile it, interleaved with the S(it + 1) MFMAs.
-    uint32_t pw[16];                           // P(it) packed to bf16 pairs
-    float ps[4];
-    auto softmax_step = [&](int q) {
-      constexpr int VPS = 32 / (2 * NDS);      // scores per MFMA step
-#pragma unroll
-      for (int v = 0; v < VPS; ++v) {
-        const int idx = q * VPS + v;           // flattened register (ks = idx / 16, r = idx % 16)
-        const float p = fast_exp2(__builtin_fmaf(sacc[idx >> 4][idx & 15], sl2, -m_use));
-        sacc[idx >> 4][idx & 15] = p;
-        ps[idx & 3] = idx < 4 ? p : ps[idx & 3] + p;
-        if (idx & 1) pw[idx >> 1] = pack_bf16x2(sacc[idx >> 4][(idx & 15) - 1], p);
-      }
-    };
-    if (it + 1 < nkv) {
-      const uint16_t* kp = kp_lane + (cur ^ 1) * (kKT * D);
-      constexpr int NQ = 2 * NDS;
-      bf16x8 kf[3];                            // K fragments, read two steps ahead
-      auto kfrag = [&](int q) {
-        return *reinterpret_cast<const bf16x8*>(kp + (q & 1) * 32 * D + koff[q >> 1]);
-      };
-      kf[0] = kfrag(0);
-      kf[1] = kfrag(1);
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int ks = q & 1, s = q >> 1;
-        if (q + 2 < NQ) kf[(q + 2) % 3] = kfrag(q + 2);
-        snext[ks] = mfma_32x32x16(kf[q % 3], qreg[s], s == 0 ? f32x16{} : snext[ks]);
-        softmax_step(q);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    } else {
-#pragma unroll
-      for (int q = 0; q < 2 * NDS; ++q) softmax_step(q);
-    }
-    lsum += (ps[0] + ps[1]) + (ps[2] + ps[3]);
-
-    // O^T (D x 32 rows) += V^T (D x 64 keys) P^T.  B operand of step (ks, st) =
-    // keys ks*32 + st*16 + half*8 + [0, 8) = packed words 8ks + 4st .. +3; the
-    // V^T operand is one 16-byte LDS read; the D/32 accumulators alternate.
-    const uint16_t* vp = vp_lane + cur * (4 * D * 16);
-    constexpr int NV = 4 * NDT;                // PV MFMAs
-    bf16x8 vf[3];                              // V^T fragments, read two MFMAs ahead
-    auto vfrag = [&](int n) {
-      return *reinterpret_cast<const bf16x8*>(vp + (n / NDT) * D * 16 + (n % NDT) * 32 * 16);
-    };
-    vf[0] = vfrag(0);
-    vf[1] = vfrag(1);
-#pragma unroll
-    for (int n = 0; n < NV; ++n) {
-      const int kst = n / NDT, dt = n % NDT;
-      if (n + 2 < NV) vf[(n + 2) % 3] = vfrag(n + 2);
-      const bf16x8 pbk = __builtin_bit_cast(
-          bf16x8, make_uint4(pw[4 * kst + 0], pw[4 * kst + 1], pw[4 * kst + 2], pw[4 * kst + 3]));
-      o[dt] = mfma_32x32x16(vf[n % 3], pbk, o[dt]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if (it + 1 < nkv) {
-      wait_vmem();                             // this wavefront's DMA of K(it + 2), V(it + 1) landed
-      fix_v(cur ^ 1, it + 1, meta_at(meta, 16 + wv));
-      __syncthreads();                         // ... and everybody's: visible, buffers free
-    }
+    wait_vmem();                               // this wavefront's DMA of K(it + 2), V(it) landed
+    fix_v(cur, it, meta_at(meta, 12 + wv));
+    __syncthreads();                           // ... and everybody's: visible, buffers free
     meta = meta_next;
   };
+  // PV of the last tile (nothing left to overlap it with).
+  auto last_pv = [&](const u32x4 (&pp)[4], int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < NSLOT; ++q) o[q % NDT] = mfma_32x32x16(vfrag(buf, q), pfrag(pp, q / NDT), o[q % NDT]);
+  };
 
-  // two tiles per trip, so the score buffers swap roles without copies
-  for (int it = 0; it < nkv; it += 2) {
-    iteration(it, sa, sb);
-    if (it + 1 < nkv) iteration(it + 1, sb, sa);
+  using T = std::true_type;
+  using F = std::false_type;
+  if (nkv == 1) {
+    step(F{}, F{}, 0, s0, s1, p1, p0);
+    last_pv(p0, 0);
+  } else {
+    step(F{}, T{}, 0, s0, s1, p1, p0);
+    int it = 1;
+    // two steps per trip while both tiles have a successor; odd tiles keep
+    // their scores / P in s1 / p1, even tiles in s0 / p0
+    for (; it + 2 < nkv; it += 2) {
+      step(T{}, T{}, it, s1, s0, p0, p1);
+      step(T{}, T{}, it + 1, s0, s1, p1, p0);
+    }
+    if (it + 1 < nkv) {                        // tiles it (odd) and it + 1 (last) remain
+      step(T{}, T{}, it, s1, s0, p0, p1);
+      step(T{}, F{}, it + 1, s0, s1, p1, p0);
+      last_pv(p0, 0);
+    } else {                                   // tile it (odd) is the last
+      step(T{}, F{}, it, s1, s0, p0, p1);
+      last_pv(p1, 1);
+    }
   }
 
   const float ltot = xhalf_sum(lsum);
