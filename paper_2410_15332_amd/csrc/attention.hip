@@ -349,10 +349,12 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
       const float p = fast_exp2(__builtin_fmaf(sc[u >> 4][u & 15], sl2, -m_use));
       sc[u >> 4][u & 15] = p;
       ps[u & 3] = u < 4 ? p : ps[u & 3] + p;
+      // Keep this unit's work in its slot: P is only read in the next step and
+      // the sums at its end, and the compiler would otherwise move all the
+      // exponentials to those first uses (and hold 32 of them live).
+      __asm__ volatile("" ::"v"(ps[u & 3]));
       if constexpr (u & 1) {
         pc[u >> 3][(u >> 1) & 3] = pack_bf16x2(sc[u >> 4][(u & 15) - 1], p);
-        // keep the pair's exponentials in this slot: P is only read in the next
-        // step, and the compiler would otherwise sink them all to that first use
         __asm__ volatile("" ::"v"(pc[u >> 3][(u >> 1) & 3]));
       }
     };
@@ -378,20 +380,29 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
           sn[k & 1] = mfma_32x32x16(kf[k % 3], qo, (k >> 1) == 0 ? f32x16{} : sn[k & 1]);
         }
       }
+      // row max over the 32 scores: four chains of three-input maxima (7 + 8 + 8
+      // + 8 scores), each step max3(running, a, b), then the chains and the lane swap
       if constexpr (q == 0) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const int ks = c >> 1, r0 = (c & 1) * 8;
-          mx[c] = fmaxf(fmaxf(fmaxf(sc[ks][r0], sc[ks][r0 + 1]), sc[ks][r0 + 2]), sc[ks][r0 + 3]);
+          mx[c] = c == 0 ? fmaxf(fmaxf(sc[0][0], sc[0][1]), sc[0][2])
+                         : fmaxf(fmaxf(mx[0], sc[ks][r0]), sc[ks][r0 + 1]);
+          if (c == 0) continue;
+          mx[c] = fmaxf(fmaxf(mx[c], sc[ks][r0 + 2]), sc[ks][r0 + 3]);
         }
       } else if constexpr (q == 1) {
+        mx[0] = fmaxf(fmaxf(mx[0], sc[0][3]), sc[0][4]);
+        mx[0] = fmaxf(fmaxf(mx[0], sc[0][5]), sc[0][6]);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const int ks = c >> 1, r0 = (c & 1) * 8 + 4;
-          mx[c] = fmaxf(fmaxf(fmaxf(mx[c], sc[ks][r0]), sc[ks][r0 + 1]), fmaxf(sc[ks][r0 + 2], sc[ks][r0 + 3]));
+        for (int c = 1; c < 4; ++c) {
+          const int ks = c >> 1, r0 = (c & 1) * 8;
+          mx[c] = fmaxf(fmaxf(mx[c], sc[ks][r0 + 4]), sc[ks][r0 + 5]);
+          mx[c] = fmaxf(fmaxf(mx[c], sc[ks][r0 + 6]), sc[ks][r0 + 7]);
         }
+        mx[0] = fmaxf(fmaxf(mx[0], sc[0][7]), mx[1]);
       } else if constexpr (q == 2) {
-        const float mt = xhalf_max(fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3])));
+        const float mt = xhalf_max(fmaxf(fmaxf(mx[0], mx[2]), mx[3]));
         m_cand = fmaxf(m, mt * sl2);
       } else if constexpr (q == 3) {
         grow = m_cand > m + kLag;              // also true on the first finite max
