@@ -95,7 +95,7 @@ typedef struct {
   int32_t n_tiles;          /* attention query tiles (per KV head) */
   int32_t n_work;           /* attention work items (per KV head) */
   int32_t n_partials;       /* split-KV partial results (per KV head) */
-  int32_t tile_rows;        /* query rows (S row x head) per tile: 128 */
+  int32_t tile_rows;        /* query rows (S row x head) per tile: 128 or 256 */
   int32_t max_pos;          /* 1 + largest linked position in the batch */
   int64_t total_ints;       /* int32 entries of the plan buffer */
 } epic_plan_sizes;

@@ -19,7 +19,7 @@ size_t round_up(size_t n, size_t a) { return (n + a - 1) / a * a; }
 
 // Workspace of the attention step: split-KV partial outputs and their log-sum-exps.
 size_t attn_partials_bytes(const epic_attn_cfg* cfg, const epic_plan_sizes* s) {
-  const size_t rows = size_t(s->n_partials) * cfg->num_kv_heads * kTileRows;
+  const size_t rows = size_t(s->n_partials) * cfg->num_kv_heads * s->tile_rows;
   return round_up(rows * cfg->head_dim * sizeof(float), 256) + round_up(rows * sizeof(float), 256);
 }
 
@@ -27,8 +27,8 @@ epic_status check_plan(const epic_plan_sizes* s, const epic_plan* p) {
   EPIC_CHECK_ARG(s != nullptr, "plan sizes are NULL");
   EPIC_CHECK_ARG(p != nullptr, "device plan is NULL");
   EPIC_CHECK_ARG(s->n_s >= 0 && s->n_work >= 0 && s->n_partials >= 0 && s->n_private >= 0, "bad plan sizes");
-  EPIC_CHECK_ARG(s->tile_rows == kTileRows, "plan was built for %d-row tiles, this library uses %d",
-                 s->tile_rows, kTileRows);
+  EPIC_CHECK_ARG(valid_tile_rows(s->tile_rows), "plan tile rows %d (expected %d or %d)", s->tile_rows,
+                 kTileRowsSmall, kTileRowsLarge);
   if (s->n_s > 0)
     EPIC_CHECK_ARG(p->s_pos && p->linked_blocks && p->block_pos0 && p->block_len && p->tiles && p->work,
                    "device plan arrays are NULL");
@@ -84,14 +84,15 @@ epic_status run_link_attention(const epic_attn_cfg* cfg, const epic_plan_sizes* 
   a.v_cache = v_cache;
   a.out = out;
   a.lse = lse;
-  const size_t rows = size_t(s->n_partials) * cfg->num_kv_heads * kTileRows;
+  const size_t rows = size_t(s->n_partials) * cfg->num_kv_heads * s->tile_rows;
   a.part_o = static_cast<float*>(workspace);
   a.part_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) +
                                         round_up(rows * cfg->head_dim * sizeof(float), 256));
   a.hq = cfg->num_q_heads;
   a.hkv = cfg->num_kv_heads;
   a.G = cfg->num_q_heads / cfg->num_kv_heads;
-  a.rows_per_tile = kTileRows / a.G;
+  a.tile_rows = s->tile_rows;
+  a.rows_per_tile = s->tile_rows / a.G;
   const float scale = cfg->softmax_scale > 0.0f ? cfg->softmax_scale : 1.0f / std::sqrt(float(cfg->head_dim));
   a.scale_log2 = scale * kLog2eHost;
   record_event(1, stream);

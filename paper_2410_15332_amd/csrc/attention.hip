@@ -7,8 +7,9 @@
 // and recomputed rows come from the private blocks written just before.
 //
 // Work decomposition (built by the host planner):
-//   tile  = 128 query rows = (S rows of one request) x (G query heads of one KV head),
-//           row t -> S row t % (128/G), head t / (128/G);
+//   tile  = T query rows (T = 128 or 256, chosen per plan) = (S rows of one
+//           request) x (G query heads of one KV head), row t -> S row t % (T/G),
+//           head t / (T/G);
 //   item  = (tile, range of linked blocks); rows whose key range spans several
 //           items get partial results (O / l, log2 l + m) merged by the combine kernel.
 // Grid = items x Hkv with blockIdx % Hkv = KV head: with 8 KV heads each XCD
@@ -16,8 +17,13 @@
 // planner orders items key-segment first, so concurrent workgroups on an XCD
 // read the same KV blocks through its L2.
 //
-// Per workgroup: 4 wavefronts x 32 rows.  Per step 64 keys (4 blocks) are
-// staged in LDS by direct buffer->LDS loads (two buffers each for K and V).
+// Per workgroup: T / 32 wavefronts x 32 rows sharing each K/V stage.  Per step
+// 64 keys (4 blocks) are staged in LDS by direct buffer->LDS loads:
+//   T = 256: one workgroup per CU, 8 wavefronts -- 0..3 load the four K blocks,
+//            4..7 the four V blocks -- three buffers each, loads issued two
+//            steps before their use;
+//   T = 128: two workgroups per CU, 4 wavefronts each loading one K and one V
+//            block, two buffers each, loads issued one step before their use.
 // S^T = K Q^T and O^T += V^T P^T run on v_mfma_f32_32x32x16_bf16: each lane
 // owns one query row (its MFMA column), so the row max / sum need a single lane
 // swap (l <-> l^32).  P is rounded to bf16 for the second product; softmax runs
@@ -38,8 +44,10 @@ namespace epic {
 
 namespace {
 
-constexpr int kKT = 64;    // keys per step (4 blocks of 16)
-constexpr int kThreads = 256;
+constexpr int kKT = 64;     // keys per step (4 blocks of 16)
+// LDS buffers per operand for W wavefronts per workgroup
+template <int W>
+constexpr int kStages = W == 8 ? 3 : 2;
 // Word 3 of a gfx9-family raw buffer descriptor (32-bit data format, no swizzle).
 constexpr int kBufWord3 = 0x00020000;
 
@@ -56,11 +64,11 @@ constexpr int kBufWord3 = 0x00020000;
 //     lane each), which would not fit in registers beside the rest.
 template <int D>
 constexpr int kQl = D == 128 ? 2 : 0;
-template <int D>
+template <int D, int W>
 struct AttnLds {
-  uint16_t k[2][kKT * D];
-  uint16_t v[2][4 * D * 16];
-  uint16_t q[kQl<D> > 0 ? kQl<D> : 1][kThreads * 8];
+  uint16_t k[kStages<W>][kKT * D];
+  uint16_t v[kStages<W>][4 * D * 16];
+  uint16_t q[kQl<D> > 0 ? kQl<D> : 1][64 * W * 8];
 };
 
 __device__ __forceinline__ int v_swz(int d) { return ((d >> 2) ^ (d >> 3)) & 1; }
@@ -74,10 +82,12 @@ typedef __attribute__((address_space(3))) void lds_void;
 template <class GOFF, int... I>
 __device__ __forceinline__ void dma_block(__amdgpu_buffer_rsrc_t rs, char* dst, int voff_even, int voff_odd,
                                           std::integer_sequence<int, I...>) {
+#if defined(__HIP_DEVICE_COMPILE__)   // the host pass only parses kernel bodies
   (__builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + 1024 * I - GOFF::template at<I>()), 16,
                                             GOFF::template odd<I>() ? voff_odd : voff_even, 0,
                                             GOFF::template at<I>(), 0),
    ...);
+#endif
 }
 // K load I of a D-wide block: row group rb = 64 I / (8 NCH), chunk base v0 = (64 I % (8 NCH)) / 8;
 // lane l reads row 8 rb + l % 8, chunk (v0 + l / 8) ^ rb.
@@ -93,6 +103,15 @@ struct VLoads {
   template <int I> static constexpr int at() { return 1024 * I; }
   template <int I> static constexpr bool odd() { return false; }
 };
+// Workgroup barrier ordering LDS accesses only: the wavefront's own LDS reads
+// and writes complete (lgkmcnt(0)) before it, and the memory clobber keeps the
+// compiler from moving or forwarding memory accesses across it, while the
+// wavefront's buffer->LDS loads still in flight stay in flight (a fence would
+// wait for them too, since they write LDS).
+__device__ __forceinline__ void barrier_lds() {
+  __asm__ volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // f(integral_constant<int, I>) for I = 0 .. N-1, every index a compile-time constant
 template <class F, int... I>
 __device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
@@ -103,8 +122,13 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-// wait until this wavefront's outstanding vector memory loads (hence its LDS DMA) are done
-__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// wait until at most N of this wavefront's vector memory loads (hence LDS DMA
+// writes) are outstanding; they complete in issue order
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
 
 // S^T row rho (0..31 inside a 32-key subtile) holds key (rho>>4)*16 + ((rho>>2)&1)*8 + ((rho>>3)&1)*4 + (rho&3).
 // With this order a lane's accumulator registers 8*st .. 8*st+7 hold the 8
@@ -124,13 +148,16 @@ __device__ __forceinline__ float xhalf_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D>
-__global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a) {
+template <int D, int W>
+__global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(AttnArgs a) {
+  constexpr int kThreads = 64 * W;
+  constexpr int S = kStages<W>;               // LDS buffers per operand
+  constexpr int TR = 32 * W;                  // tile rows
   constexpr int NDS = D / 16;                 // k-steps of S^T = K Q^T
   constexpr int NDT = D / 32;                 // 32-row tiles of O^T
   constexpr int NSLOT = 2 * NDS;              // QK MFMAs per tile (= PV MFMAs, 4 * NDT)
   static_assert(NSLOT == 4 * NDT, "QK and PV MFMA counts pair up");
-  __shared__ __attribute__((aligned(16))) AttnLds<D> lds;
+  __shared__ __attribute__((aligned(16))) AttnLds<D, W> lds;
 
   const int hkv = a.hkv;
   const int g = blockIdx.x % hkv;
@@ -172,9 +199,13 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   };
 
   const int nkv = (b1 - b0 + 3) / 4;
-  // Wavefront w stages block w of each KV tile: its 16 K rows and its [D][16]
-  // V slab, D/32 loads of 1 KB each, through a descriptor over that block.
+  // Block dw of each KV tile is staged by this wavefront: its 16 K rows (k_wave)
+  // and / or its [D][16] V slab (v_wave), D/32 loads of 1 KB each through a
+  // descriptor over that block.  W = 8: wavefronts 0..3 K, 4..7 V; W = 4: both.
   const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int dw = wv & 3;
+  const bool k_wave = W == 4 || wv < 4;
+  const bool v_wave = W == 4 || wv >= 4;
   constexpr int NI = D / 32;                  // 1 KB loads per operand per wavefront
   constexpr int NCH = D / 8;                  // 16-byte chunks per K row
   const char* kbase = reinterpret_cast<const char*>(a.k_cache + size_t(g) * 16 * D);
@@ -190,32 +221,33 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   auto dma_k = [&](int buf, int phys) {
     const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(kbase) + size_t(phys) * blk_bytes, 0,
                                                       16 * D * 2, kBufWord3);
-    dma_block<KLoads<D>>(rs, reinterpret_cast<char*>(&lds.k[buf][16 * wv * D]), kvo, kvo ^ 16,
+    dma_block<KLoads<D>>(rs, reinterpret_cast<char*>(&lds.k[buf][16 * dw * D]), kvo, kvo ^ 16,
                          std::make_integer_sequence<int, NI>{});
   };
   auto dma_v = [&](int buf, int phys) {
     const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(vbase) + size_t(phys) * blk_bytes, 0,
                                                       16 * D * 2, kBufWord3);
-    dma_block<VLoads>(rs, reinterpret_cast<char*>(&lds.v[buf][wv * D * 16]), vvo, vvo,
+    dma_block<VLoads>(rs, reinterpret_cast<char*>(&lds.v[buf][dw * D * 16]), vvo, vvo,
                       std::make_integer_sequence<int, NI>{});
   };
 
-  // Block metadata of step t, gathered one step ahead into lanes of one
-  // register (a vector load that lands with that step's DMA):
-  //   lanes  0..3 : physical ids of tile t + 2 (K DMA in step t)
-  //   lanes  4..7 : physical ids of tile t     (V DMA in step t)
-  //   lanes  8..11: first positions of tile t's blocks (mask of tile t)
-  //   lanes 12..15: valid slots of tile t's blocks, 0 past b1 (mask, V fix-up)
-  const int mj = lane & 31;
-  const int m_kind = mj < 8 ? 0 : (mj < 12 ? 1 : 2);
-  const int m_toff = mj < 4 ? 2 : 0;
-  const int32_t* m_arr = m_kind == 0 ? a.linked_blocks : (m_kind == 1 ? a.block_pos0 : a.block_len);
-  auto load_meta = [&](int ts) -> int {
-    const int blk = b0 + 4 * (ts + m_toff) + (mj & 3);
-    const int x = m_arr[max(b0, min(blk, b1 - 1))];   // tiles before 0 / past b1 stay in range
-    return (m_kind == 2 && blk >= b1) ? 0 : x;
+  // Block metadata, read with scalar loads: the tables are read-only while the
+  // kernel runs, and scalar loads are counted by lgkmcnt, so waiting for them
+  // never waits for the buffer->LDS loads in flight.  Indices are clamped into
+  // the item's range [b0, b1).
+  typedef __attribute__((address_space(4))) const int32_t cint32;
+  const cint32* lb_c = (const cint32*)a.linked_blocks;
+  const cint32* pos_c = (const cint32*)a.block_pos0;
+  const cint32* len_c = (const cint32*)a.block_len;
+  auto blk_at = [&](const cint32* arr, int i) -> int { return arr[max(b0, min(i, b1 - 1))]; };
+  // physical ids this wavefront stages in step ts: K(ts + S) and V(ts + S - 2), block dw
+  auto phys_k = [&](int ts) -> int { return blk_at(lb_c, b0 + 4 * (ts + S) + dw); };
+  auto phys_v = [&](int ts) -> int { return blk_at(lb_c, b0 + 4 * (ts + S - 2) + dw); };
+  // first position / valid slots of block beta of tile ts (0 slots past b1)
+  auto blk_pos = [&](int ts, int beta) -> int { return blk_at(pos_c, b0 + 4 * ts + beta); };
+  auto blk_len = [&](int ts, int beta) -> int {
+    return b0 + 4 * ts + beta < b1 ? blk_at(len_c, b0 + 4 * ts + beta) : 0;
   };
-  auto meta_at = [&](int meta, int k) -> int { return __builtin_amdgcn_readlane(meta, k); };
 
   // After this wavefront's V DMA of tile `it` landed: zero the slots past its
   // block's end (partial or absent block), so stale or NaN bits never meet a
@@ -225,7 +257,7 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
 #pragma unroll
     for (int i = 0; i < D / 64; ++i) {
       const int d = lane + 64 * i;
-      uint16_t* row = &lds.v[buf][(wv * D + d) * 16];
+      uint16_t* row = &lds.v[buf][(dw * D + d) * 16];
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         uint4* q = reinterpret_cast<uint4*>(row + (hf ^ v_swz(d)) * 8);
@@ -275,15 +307,24 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
   auto pfrag = [&](const u32x4 (&p)[4], int kst) { return __builtin_bit_cast(bf16x8, p[kst]); };
 
-  int meta = 0;                                // metadata of the current step
-  {
-    const int pro = load_meta(-1);             // lanes 0..3: ids of tile 1
-    meta = load_meta(0);                       // lanes 4..7: ids of tile 0
-    wait_vmem();
-    dma_k(0, meta_at(meta, 4 + wv));
-    if (nkv > 1) dma_k(1, meta_at(pro, wv));
-    wait_vmem();
+  // Pipeline: K(t) and V(t) live in LDS buffer t % S.  Step t reads K(t + 1)
+  // and V(t - 1), and issues K(t + S) and V(t + S - 2) into the buffers whose
+  // last readers ran in step t - 1; at its end every wavefront waits for its
+  // loads of K(t + 2) and V(t) -- with S = 3 those were issued a step earlier,
+  // and the loads of this step stay in flight -- and the barrier publishes
+  // them.  The loads are issued every step (past the item's end with clamped
+  // block ids), so each step leaves exactly NI loads outstanding (S = 3).
+  if (k_wave) {                                // K(0) .. K(S - 1)
+#pragma unroll
+    for (int j = 0; j < S; ++j) dma_k(j, phys_k(j - S));
   }
+  if (v_wave) {                                // V(0) .. V(S - 3)
+#pragma unroll
+    for (int j = 0; j < S - 2; ++j) dma_v(j, phys_v(j - S + 2));
+  }
+  int pk = phys_k(0), pv = phys_v(0);          // blocks this wavefront stages in the current step
+  wait_vmem<0>();
+  if (S == 3 && v_wave) fix_v(0, 0, blk_len(0, dw));
   __syncthreads();
 
   f32x16 s0[2], s1[2];                         // scores of even / odd tiles
@@ -293,7 +334,7 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
     const int ks = q & 1, s = q >> 1;
     s0[ks] = mfma_32x32x16(kfrag(0, q), qfrag(s), s == 0 ? f32x16{} : s0[ks]);
   }
-  __syncthreads();                             // K buffer 0 is rewritten in step 0
+  __syncthreads();                             // K buffer 0 is rewritten in step 0 (K(S))
 
   // One step over tile it.  sc = S(it) on entry (complete); pp = P(it - 1) (PV
   // only); the step leaves P(it) in pc and S(it + 1) in sn (QK only).
@@ -301,10 +342,13 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
                   const u32x4 (&pp)[4], u32x4 (&pc)[4]) __attribute__((always_inline)) {
     constexpr bool PV = decltype(pv_tag)::value;
     constexpr bool QK = decltype(qk_tag)::value;
-    const int cur = it & 1;
-    if (it + 2 < nkv) dma_k(cur, meta_at(meta, wv));          // K(it + 2): its buffer held K(it)
-    dma_v(cur, meta_at(meta, 4 + wv));                         // V(it): its buffer held V(it - 2)
-    const int meta_next = load_meta(it + 1);                   // lands with this step's DMA
+    const int b3 = it % S;                     // buffer of K(it), V(it), K(it + S)
+    const int b3n = b3 == S - 1 ? 0 : b3 + 1;  // buffer of K(it + 1) (and V(it + 1) when S = 3)
+    const int b3p = b3 == 0 ? S - 1 : b3 - 1;  // buffer of V(it - 1)
+    if (k_wave) dma_k(b3, pk);                                 // K(it + S): its buffer held K(it)
+    if (v_wave) dma_v(S == 3 ? b3n : b3, pv);                  // V(it + S - 2): its buffer held V(it - 2)
+    const int pk_next = k_wave ? phys_k(it + 1) : 0;
+    const int pv_next = v_wave ? phys_v(it + 1) : 0;
 
     // Mask: only tiles past the item's unmasked prefix (diagonal, partial blocks).
     // Register r = i*4 + j of subtile ks holds key ks*32 + (i>>1)*16 + half*8 + (i&1)*4 + j.
@@ -312,8 +356,8 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
       int bpos0[4], blen[4];
 #pragma unroll
       for (int beta = 0; beta < 4; ++beta) {
-        bpos0[beta] = meta_at(meta, 8 + beta);
-        blen[beta] = meta_at(meta, 12 + beta);
+        bpos0[beta] = blk_pos(it, beta);
+        blen[beta] = blk_len(it, beta);
       }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
@@ -327,12 +371,11 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
         }
     }
 
-    const int rb = cur ^ 1;                    // buffers read in this step: K(it + 1), V(it - 1)
     bf16x8 kf[3], vf[3], qf[2];                // operands, read two MFMAs ahead
-    if (PV) { vf[0] = vfrag(rb, 0); vf[1] = vfrag(rb, 1); }
+    if (PV) { vf[0] = vfrag(b3p, 0); vf[1] = vfrag(b3p, 1); }
     if (!PV && QK) {
-      kf[0] = kfrag(rb, 0);
-      kf[1] = kfrag(rb, 1);
+      kf[0] = kfrag(b3n, 0);
+      kf[1] = kfrag(b3n, 1);
     }
 
     float mx[4], m_cand = 0.0f, alpha = 1.0f, m_use = 0.0f;
@@ -361,11 +404,11 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
     static_for<NS2>([&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
       if constexpr (q + 2 < NSLOT) {
-        if constexpr (PV) vf[(q + 2) % 3] = vfrag(rb, q + 2);
+        if constexpr (PV) vf[(q + 2) % 3] = vfrag(b3p, q + 2);
       } else if constexpr (q + 2 < NS2) {
         constexpr int k2 = q + 2 - NSLOT;
         if constexpr (QK && (PV || k2 >= 2)) {
-          kf[k2 % 3] = kfrag(rb, k2);
+          kf[k2 % 3] = kfrag(b3n, k2);
           if constexpr ((k2 & 1) == 0 && (k2 >> 1) >= NQR) qf[((k2 >> 1) - NQR) & 1] = qfrag(k2 >> 1);
         }
       }
@@ -423,10 +466,11 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
     }
-    wait_vmem();                               // this wavefront's DMA of K(it + 2), V(it) landed
-    fix_v(cur, it, meta_at(meta, 12 + wv));
-    __syncthreads();                           // ... and everybody's: visible, buffers free
-    meta = meta_next;
+    wait_vmem<S == 3 ? NI : 0>();              // this wavefront's loads of K(it + 2), V(it)
+    if (v_wave) fix_v(b3, it, blk_len(it, dw));
+    barrier_lds();                             // ... of every wavefront: visible, buffers free
+    pk = pk_next;
+    pv = pv_next;
   };
   // PV of the last tile (nothing left to overlap it with).
   auto last_pv = [&](const u32x4 (&pp)[4], int buf) __attribute__((always_inline)) {
@@ -451,12 +495,13 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
     if (it + 1 < nkv) {                        // tiles it (odd) and it + 1 (last) remain
       step(T{}, T{}, it, s1, s0, p0, p1);
       step(T{}, F{}, it + 1, s0, s1, p1, p0);
-      last_pv(p0, 0);
+      last_pv(p0, (it + 1) % S);
     } else {                                   // tile it (odd) is the last
       step(T{}, F{}, it, s1, s0, p0, p1);
-      last_pv(p1, 1);
+      last_pv(p1, it % S);
     }
   }
+  wait_vmem<0>();                              // the last step's loads land before the LDS is released
 
   const float ltot = xhalf_sum(lsum);
   if (!row_ok) return;
@@ -474,7 +519,7 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
       }
     if (a.lse && half == 0) a.lse[size_t(srow) * a.hq + h] = (m + fast_log2(ltot)) * kLn2;
   } else {
-    float* pp = a.part_o + ((size_t(part) * hkv + g) * 128 + t) * D + half * 4;
+    float* pp = a.part_o + ((size_t(part) * hkv + g) * TR + t) * D + half * 4;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -484,15 +529,16 @@ __global__ __launch_bounds__(kThreads, 2) void link_attention_kernel(AttnArgs a)
         *reinterpret_cast<float4*>(pp + dt * 32 + i * 8) = f;
       }
     if (half == 0)
-      a.part_lse[(size_t(part) * hkv + g) * 128 + t] = ltot > 0.0f ? m + fast_log2(ltot) : -INFINITY;
+      a.part_lse[(size_t(part) * hkv + g) * TR + t] = ltot > 0.0f ? m + fast_log2(ltot) : -INFINITY;
   }
 }
 
 // Merge the split-KV partials of a tile: lse = log2 sum_i 2^lse_i, out = sum_i 2^(lse_i - lse) O_i.
-// Workgroup = (tile, KV head, quarter of the head dim); thread = (tile row, 16 dims).
+// Workgroup = (tile, KV head, quarter of the head dim); thread = (tile row, half of that quarter).
 constexpr int kCombineParts = 4;
+constexpr int kCombineThreads = 512;   // 2 x the largest tile
 template <int D>
-__global__ __launch_bounds__(kThreads) void link_combine_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kCombineThreads) void link_combine_kernel(AttnArgs a) {
   constexpr int DQ = D / kCombineParts;       // dims per workgroup
   constexpr int DT = DQ / 2;                  // dims per thread (16 or 8)
   const int hkv = a.hkv;
@@ -504,22 +550,24 @@ __global__ __launch_bounds__(kThreads) void link_combine_kernel(AttnArgs a) {
   if (p0 < 0) return;
   const int row0 = a.tiles[4 * tile + 0], nrows = a.tiles[4 * tile + 1];
   const int t = threadIdx.x >> 1, hf = threadIdx.x & 1;
+  const int TR = a.tile_rows;
+  if (t >= TR) return;
   const int R = a.rows_per_tile;
   const int srl = t % R, h = g * a.G + t / R;
   if (srl >= nrows) return;
   const int srow = row0 + srl;
   const int d0 = dq * DQ + hf * DT;
   float mx = -INFINITY;
-  for (int i = 0; i < ns; ++i) mx = fmaxf(mx, a.part_lse[(size_t(p0 + i) * hkv + g) * 128 + t]);
+  for (int i = 0; i < ns; ++i) mx = fmaxf(mx, a.part_lse[(size_t(p0 + i) * hkv + g) * TR + t]);
   float acc[DT];
 #pragma unroll
   for (int d = 0; d < DT; ++d) acc[d] = 0.0f;
   float wsum = 0.0f;
   for (int i = 0; i < ns; ++i) {
-    const float l = a.part_lse[(size_t(p0 + i) * hkv + g) * 128 + t];
+    const float l = a.part_lse[(size_t(p0 + i) * hkv + g) * TR + t];
     const float w = fast_exp2(l - mx);
     wsum += w;
-    const float* pp = a.part_o + ((size_t(p0 + i) * hkv + g) * 128 + t) * D + d0;
+    const float* pp = a.part_o + ((size_t(p0 + i) * hkv + g) * TR + t) * D + d0;
 #pragma unroll
     for (int d = 0; d < DT; d += 4) {
       const float4 f = *reinterpret_cast<const float4*>(pp + d);
@@ -548,19 +596,26 @@ __global__ __launch_bounds__(kThreads) void link_combine_kernel(AttnArgs a) {
 void launch_link_attention(const AttnArgs& a, int head_dim, int n_work, hipStream_t stream) {
   if (n_work == 0) return;
   const dim3 grid(unsigned(n_work) * unsigned(a.hkv));
-  if (head_dim == 128)
-    link_attention_kernel<128><<<grid, kThreads, 0, stream>>>(a);
-  else
-    link_attention_kernel<64><<<grid, kThreads, 0, stream>>>(a);
+  if (a.tile_rows == 256) {
+    if (head_dim == 128)
+      link_attention_kernel<128, 8><<<grid, 512, 0, stream>>>(a);
+    else
+      link_attention_kernel<64, 8><<<grid, 512, 0, stream>>>(a);
+  } else {
+    if (head_dim == 128)
+      link_attention_kernel<128, 4><<<grid, 256, 0, stream>>>(a);
+    else
+      link_attention_kernel<64, 4><<<grid, 256, 0, stream>>>(a);
+  }
 }
 
 void launch_link_combine(const AttnArgs& a, int head_dim, int n_tiles, hipStream_t stream) {
   if (n_tiles == 0) return;
   const dim3 grid(unsigned(n_tiles) * unsigned(a.hkv) * kCombineParts);
   if (head_dim == 128)
-    link_combine_kernel<128><<<grid, kThreads, 0, stream>>>(a);
+    link_combine_kernel<128><<<grid, kCombineThreads, 0, stream>>>(a);
   else
-    link_combine_kernel<64><<<grid, kThreads, 0, stream>>>(a);
+    link_combine_kernel<64><<<grid, kCombineThreads, 0, stream>>>(a);
 }
 
 }  // namespace epic

@@ -26,9 +26,10 @@ struct AttnArgs {
   const uint16_t* v_cache;
   uint16_t* out;            // [n_s][hq][D]
   float* lse;               // [n_s][hq] or null
-  float* part_o;            // [n_partials][hkv][128][D]
-  float* part_lse;          // [n_partials][hkv][128], log2 domain
+  float* part_o;            // [n_partials][hkv][tile_rows][D]
+  float* part_lse;          // [n_partials][hkv][tile_rows], log2 domain
   int hq, hkv, G, rows_per_tile;
+  int tile_rows;            // 128 or 256 (selects the kernel)
   float scale_log2;         // softmax scale * log2(e)
 };
 

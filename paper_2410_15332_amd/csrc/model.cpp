@@ -143,7 +143,7 @@ epic_status check_common(const epic_model_cfg* c, const epic_plan_sizes* s, cons
   epic_status st = validate_model(c);
   if (st != EPIC_OK) return st;
   EPIC_CHECK_ARG(s && p, "plan is NULL");
-  EPIC_CHECK_ARG(s->tile_rows == kTileRows, "plan tile rows mismatch");
+  EPIC_CHECK_ARG(valid_tile_rows(s->tile_rows), "plan tile rows %d unsupported", s->tile_rows);
   if (s->n_s == 0) return EPIC_OK;
   EPIC_CHECK_ARG(p->s_pos && p->tiles && p->work && p->linked_blocks, "device plan arrays are NULL");
   EPIC_CHECK_ARG(h != nullptr && (reinterpret_cast<uintptr_t>(h) & 15u) == 0, "hidden_s must be 16-byte aligned");

@@ -8,6 +8,7 @@
 // work decomposition (query tiles x split-KV key ranges).
 #include <algorithm>
 #include <cstring>
+#include <functional>
 #include <vector>
 
 #include "plan_internal.h"
@@ -21,8 +22,9 @@ epic_status validate_attn_cfg(const epic_attn_cfg* cfg) {
     return fail(EPIC_ERR_INVALID_ARG, "num_q_heads (%d) must be a positive multiple of num_kv_heads (%d)",
                 cfg->num_q_heads, cfg->num_kv_heads);
   const int G = cfg->num_q_heads / cfg->num_kv_heads;
-  if ((G & (G - 1)) != 0 || G > kTileRows)
-    return fail(EPIC_ERR_UNSUPPORTED, "query heads per KV head (%d) must be a power of two <= %d", G, kTileRows);
+  if ((G & (G - 1)) != 0 || G > kTileRowsSmall)
+    return fail(EPIC_ERR_UNSUPPORTED, "query heads per KV head (%d) must be a power of two <= %d", G,
+                kTileRowsSmall);
   if (cfg->head_dim != 64 && cfg->head_dim != 128)
     return fail(EPIC_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", cfg->head_dim);
   if (cfg->block_size != kBlock)
@@ -129,25 +131,98 @@ void make_tiles(const epic_link_request* reqs, int batch, int rows_per_tile, std
   }
 }
 
-// Key blocks per split-KV work item.  Rows are split only as far as needed to
-// give about kTargetItems workgroups (four per workgroup slot of 256 CUs x 2),
-// halving from "no split"; a split never goes below 64 blocks (1024 keys):
-// every split writes and re-reads a 128-row fp32 partial result, which must
-// stay small next to the attention work of the item.
-int split_blocks(const epic_attn_cfg* cfg, const std::vector<Tile>& tiles) {
-  if (cfg->kv_split_blocks > 0) return std::max(kKvTileBlocks, cfg->kv_split_blocks / kKvTileBlocks * kKvTileBlocks);
-  constexpr int64_t kTargetItems = 2048;
+// Work items of a split, in launch order: segment-major (all first segments,
+// then all second segments, ...), and within a segment the tiles with the
+// longest key range first.  Each entry: (tile, segment).
+std::vector<std::pair<int, int>> item_order(const std::vector<Tile>& tiles, int split) {
+  std::vector<int> order(tiles.size());
+  for (size_t t = 0; t < tiles.size(); ++t) order[t] = static_cast<int>(t);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return tiles[x].nblk > tiles[y].nblk; });
+  int max_splits = 1;
+  for (const Tile& t : tiles) max_splits = std::max(max_splits, cdiv(t.nblk, split));
+  std::vector<std::pair<int, int>> items;
+  for (int seg = 0; seg < max_splits; ++seg)
+    for (int t : order)
+      if (seg < std::max(1, cdiv(tiles[t].nblk, split))) items.emplace_back(t, seg);
+  return items;
+}
+
+// Kernel shape of a tile size: workgroup slots per launch round, and the time of
+// one 64-key step of one workgroup and its fixed prologue / epilogue charge, in
+// steps (the split search compares splits of one shape only).
+// A split item also writes its fp32 partial tile, which the combine reads back.
+struct TileShape {
+  int rows, slots;
+  double step_cost, item_overhead, partial_cost;
+};
+constexpr TileShape kShapeLarge{kTileRowsLarge, 256, 1.0, 3.0, 1.5};   // one 8-wavefront workgroup per CU, 256 CUs
+constexpr TileShape kShapeSmall{kTileRowsSmall, 512, 1.0, 2.0, 1.5};   // two 4-wavefront workgroups per CU
+
+// Estimated duration of the attention launch for a split: the items (times the
+// KV heads, head-minor as in the grid) are dealt in launch order to the
+// workgroup slots, each to the slot that frees up first -- as the hardware
+// dispatcher does -- and an item costs its steps plus a fixed prologue /
+// epilogue charge.
+double estimate_makespan(const std::vector<Tile>& tiles, int split, int hkv, const TileShape& sh) {
+  std::vector<double> slots(sh.slots, 0.0);   // min-heap of slot finish times
+  double makespan = 0.0;
+  for (const auto& [t, seg] : item_order(tiles, split)) {
+    const int blocks = std::min(tiles[t].nblk, (seg + 1) * split) - seg * split;
+    const bool partial = tiles[t].nblk > split;
+    const double cost = cdiv(std::max(blocks, 1), kKvTileBlocks) * sh.step_cost + sh.item_overhead +
+                        (partial ? sh.partial_cost : 0.0);
+    for (int g = 0; g < hkv; ++g) {
+      std::pop_heap(slots.begin(), slots.end(), std::greater<double>());
+      slots.back() += cost;
+      makespan = std::max(makespan, slots.back());
+      std::push_heap(slots.begin(), slots.end(), std::greater<double>());
+    }
+  }
+  return makespan;
+}
+
+// Key blocks per split-KV work item: among splits max_nblk / n (n from 1 to 128
+// in about geometric steps, rounded up to whole 4-block tiles, never below 64
+// blocks, because every split writes and re-reads a tile of fp32 partial
+// results), the one with the shortest estimated launch; ties go to the larger
+// split (fewer partials).  *time receives that estimate.
+int split_blocks(const epic_attn_cfg* cfg, const std::vector<Tile>& tiles, const TileShape& sh, double* time) {
+  const int hkv = cfg->num_kv_heads;
+  if (cfg->kv_split_blocks > 0) {
+    const int split = std::max(kKvTileBlocks, cfg->kv_split_blocks / kKvTileBlocks * kKvTileBlocks);
+    *time = estimate_makespan(tiles, split, hkv, sh);
+    return split;
+  }
   constexpr int kMinSplit = 64;
+  constexpr int64_t kMaxRounds = 16;   // past this many dispatch rounds, splitting cannot balance better
   int max_nblk = kKvTileBlocks;
   for (const Tile& t : tiles) max_nblk = std::max(max_nblk, t.nblk);
-  int split = (max_nblk + kKvTileBlocks - 1) / kKvTileBlocks * kKvTileBlocks;
-  while (split > kMinSplit) {
-    int64_t items = 0;
-    for (const Tile& t : tiles) items += std::max(1, cdiv(t.nblk, split));
-    if (items * cfg->num_kv_heads >= kTargetItems) break;
-    split = std::max(kMinSplit, (split / 2 + kKvTileBlocks - 1) / kKvTileBlocks * kKvTileBlocks);
+  auto n_items = [&](int split) {
+    int64_t n = 0;
+    for (const Tile& t : tiles) n += std::max(1, cdiv(t.nblk, split));
+    return n;
+  };
+  const int whole = cdiv(max_nblk, kKvTileBlocks) * kKvTileBlocks;
+  int best = whole;
+  double best_time = estimate_makespan(tiles, whole, hkv, sh);
+  if (n_items(whole) * hkv < kMaxRounds * sh.slots) {
+    int prev = whole;
+    static constexpr int kParts[] = {2, 3, 4, 5, 6, 7, 8, 10, 12, 14, 16, 20, 24, 28, 32, 40, 48, 56, 64, 96, 128};
+    for (const int n : kParts) {
+      const int split = std::max(kMinSplit, cdiv(cdiv(max_nblk, n), kKvTileBlocks) * kKvTileBlocks);
+      if (split >= prev) continue;
+      prev = split;
+      if (n_items(split) * hkv > kMaxRounds * sh.slots) break;
+      const double t = estimate_makespan(tiles, split, hkv, sh);
+      if (t < best_time * 0.999) {
+        best_time = t;
+        best = split;
+      }
+      if (split == kMinSplit) break;
+    }
   }
-  return split;
+  *time = best_time;
+  return best;
 }
 
 int64_t align16(int64_t n) { return (n + 15) & ~int64_t(15); }
@@ -158,10 +233,12 @@ int64_t align16(int64_t n) { return (n + 15) & ~int64_t(15); }
 
 using namespace epic;
 
-extern "C" epic_status epic_plan_sizes_get(const epic_link_request* reqs, int32_t batch,
-                                           const epic_attn_cfg* cfg, int32_t n_free,
-                                           epic_plan_sizes* out) {
-  clear_error();
+namespace {
+
+// Sizes of the plan, plus its attention tiles and split (shared by the sizes
+// query and the plan builder, so the split search runs once per call).
+epic_status plan_shape(const epic_link_request* reqs, int32_t batch, const epic_attn_cfg* cfg, int32_t n_free,
+                       epic_plan_sizes* out, std::vector<Tile>* tiles_out, int* split_out) {
   EPIC_CHECK_ARG(out != nullptr, "output sizes pointer is NULL");
   EPIC_CHECK_ARG(batch >= 0, "batch %d < 0", batch);
   EPIC_CHECK_ARG(batch == 0 || reqs != nullptr, "requests pointer is NULL");
@@ -170,7 +247,6 @@ extern "C" epic_status epic_plan_sizes_get(const epic_link_request* reqs, int32_
   if (st != EPIC_OK) return st;
   epic_plan_sizes s{};
   s.batch = batch;
-  s.tile_rows = kTileRows;
   int64_t n_s = 0, n_lb = 0, n_priv = 0, max_pos = 0;
   for (int b = 0; b < batch; ++b) {
     ReqShape sh;
@@ -184,11 +260,37 @@ extern "C" epic_status epic_plan_sizes_get(const epic_link_request* reqs, int32_
   EPIC_CHECK_ARG(n_s < (int64_t(1) << 30) && n_lb < (int64_t(1) << 30), "batch too large");
   if (n_priv > n_free)
     return fail(EPIC_ERR_NO_PRIVATE_BLOCKS, "plan needs %lld private blocks, %d free", (long long)n_priv, n_free);
+  // Tile size.  256-row tiles share each staged K/V block between twice the
+  // rows, which pays when their rows need the same keys: take them when they
+  // cost at most 1% more (row x 64-key) steps than 128-row tiles -- rows of
+  // one stretch of positions (recompute-all, suffix-only) rather than the
+  // first k rows of several chunks -- and still give every CU a workgroup.
   const int G = cfg->num_q_heads / cfg->num_kv_heads;
-  std::vector<Tile> tiles;
+  std::vector<Tile>& tiles = *tiles_out;
+  std::vector<Tile> small, large;
   int64_t total_blocks = 0;
-  make_tiles(reqs, batch, kTileRows / G, &tiles, &total_blocks);
-  const int split = split_blocks(cfg, tiles);
+  make_tiles(reqs, batch, kTileRowsSmall / G, &small, &total_blocks);
+  make_tiles(reqs, batch, kTileRowsLarge / G, &large, &total_blocks);
+  auto row_steps = [](const std::vector<Tile>& ts, int rows) {
+    int64_t n = 0;
+    for (const Tile& t : ts) n += int64_t(cdiv(t.nblk, kKvTileBlocks)) * rows;
+    return n;
+  };
+  double est = 0.0;
+  int split = split_blocks(cfg, large, kShapeLarge, &est);
+  int64_t large_items = 0;
+  for (const Tile& t : large) large_items += std::max(1, cdiv(t.nblk, split));
+  const bool use_large = row_steps(large, kTileRowsLarge) * 100 <= row_steps(small, kTileRowsSmall) * 101 &&
+                         large_items * cfg->num_kv_heads >= kShapeLarge.slots;
+  if (use_large) {
+    tiles.swap(large);
+    s.tile_rows = kTileRowsLarge;
+  } else {
+    tiles.swap(small);
+    s.tile_rows = kTileRowsSmall;
+    split = split_blocks(cfg, tiles, kShapeSmall, &est);
+  }
+  *split_out = split;
   int64_t n_work = 0, n_part = 0;
   for (const Tile& t : tiles) {
     const int ns = std::max(1, cdiv(t.nblk, split));
@@ -206,6 +308,17 @@ extern "C" epic_status epic_plan_sizes_get(const epic_link_request* reqs, int32_
                  align16(n_priv * kBlock) + align16(4 * int64_t(tiles.size())) + align16(kWorkInts * n_work);
   *out = s;
   return EPIC_OK;
+}
+
+}  // namespace
+
+extern "C" epic_status epic_plan_sizes_get(const epic_link_request* reqs, int32_t batch,
+                                           const epic_attn_cfg* cfg, int32_t n_free,
+                                           epic_plan_sizes* out) {
+  clear_error();
+  std::vector<Tile> tiles;
+  int split = 0;
+  return plan_shape(reqs, batch, cfg, n_free, out, &tiles, &split);
 }
 
 extern "C" epic_status epic_plan_layout(const epic_plan_sizes* s, int32_t* base, epic_plan* p) {
@@ -238,8 +351,11 @@ extern "C" epic_status epic_plan_link(const epic_link_request* reqs, int32_t bat
                                       const epic_attn_cfg* cfg, const int32_t* free_blocks,
                                       int32_t n_free, int32_t num_blocks,
                                       const epic_plan_sizes* sizes, epic_plan* plan) {
+  clear_error();
   epic_plan_sizes chk;
-  epic_status st = epic_plan_sizes_get(reqs, batch, cfg, n_free, &chk);
+  std::vector<Tile> tiles;
+  int split = 0;
+  epic_status st = plan_shape(reqs, batch, cfg, n_free, &chk, &tiles, &split);
   if (st != EPIC_OK) return st;
   EPIC_CHECK_ARG(sizes && plan, "NULL sizes or plan");
   EPIC_CHECK_ARG(std::memcmp(&chk, sizes, sizeof(chk)) == 0, "sizes do not match these requests");
@@ -337,31 +453,20 @@ extern "C" epic_status epic_plan_link(const epic_link_request* reqs, int32_t bat
   // Attention tiles and split-KV work items.  Work items are ordered key
   // segment first, so that the workgroups running at the same time read the
   // same KV blocks (one L2 per XCD serves them).
-  const int G = cfg->num_q_heads / cfg->num_kv_heads;
-  std::vector<Tile> tiles;
-  int64_t total_blocks = 0;
-  make_tiles(reqs, batch, kTileRows / G, &tiles, &total_blocks);
-  const int split = split_blocks(cfg, tiles);
-  int part = 0, max_splits = 1;
+  int part = 0;
   for (size_t t = 0; t < tiles.size(); ++t) {
     const int ns = std::max(1, cdiv(tiles[t].nblk, split));
-    max_splits = std::max(max_splits, ns);
     plan->tiles[4 * t + 0] = tiles[t].row0;
     plan->tiles[4 * t + 1] = tiles[t].nrows;
     plan->tiles[4 * t + 2] = ns > 1 ? part : -1;
     plan->tiles[4 * t + 3] = ns;
     if (ns > 1) part += ns;
   }
-  // inside a segment, tiles with the longest key range go first (the tail of
-  // the launch then holds the short items)
-  std::vector<int> order(tiles.size());
-  for (size_t t = 0; t < tiles.size(); ++t) order[t] = static_cast<int>(t);
-  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return tiles[x].nblk > tiles[y].nblk; });
+  // work items in launch order (segment-major, longest key range first)
   int w = 0;
-  for (int seg = 0; seg < max_splits; ++seg) {
-    for (int t : order) {
+  for (const auto& [t, seg] : item_order(tiles, split)) {
+    {
       const int ns = plan->tiles[4 * t + 3];
-      if (seg >= ns) continue;
       const int base = plan->blk_off[tiles[t].req];
       const int b0 = base + seg * split;
       const int b1 = base + std::min(tiles[t].nblk, (seg + 1) * split);

@@ -6,7 +6,11 @@
 namespace epic {
 
 constexpr int kBlock = 16;         // token slots per KV block
-constexpr int kTileRows = 128;     // (S row, query head) pairs per attention tile
+// (S row, query head) pairs per attention tile: 128 (two 4-wavefront workgroups per
+// CU) or 256 (one 8-wavefront workgroup per CU), chosen per plan by the planner
+constexpr int kTileRowsSmall = 128;
+constexpr int kTileRowsLarge = 256;
+inline bool valid_tile_rows(int r) { return r == kTileRowsSmall || r == kTileRowsLarge; }
 constexpr int kKvTileBlocks = 4;   // KV blocks staged per attention iteration (64 keys)
 constexpr int kWorkInts = 8;       // int32 per attention work item
 constexpr float kLog2eHost = 1.442695040888963407f;

@@ -98,7 +98,7 @@ def test_work_items_cover_causal_ranges():
     reqs, n_used = _random_requests(rng, 3, max_chunks=8, max_len=300)
     for split in (0, 4, 16):
         cfg, sizes, v, _ = _plan(reqs, n_used, 32, 8, split=split)
-        R = 128 // 4
+        R = sizes.tile_rows // 4
         tiles = v["tiles"].reshape(-1, 4)
         work = v["work"].reshape(-1, el.WORK_INTS)
         # tiles cover S in order with at most R rows each
