@@ -62,7 +62,9 @@ const char* epic_version(void);
  * power of two <= 128.  Query head h reads KV head floor(h / G).
  * softmax_scale == 0 means 1 / sqrt(head_dim).
  * kv_split_blocks: key blocks per split-KV work item (0 = library default);
- * rows whose keys span several work items are merged with a log-sum-exp combine. */
+ * rows whose keys span several work items are merged with a log-sum-exp combine.
+ * tile_rows: query rows (S row x head) per attention workgroup, 128 or 256
+ * (0 = library default: 256 when the rows of a tile need nearly the same keys). */
 typedef struct {
   int32_t num_q_heads;
   int32_t num_kv_heads;
@@ -70,6 +72,7 @@ typedef struct {
   int32_t block_size;
   float softmax_scale;
   int32_t kv_split_blocks;
+  int32_t tile_rows;
 } epic_attn_cfg;
 
 /* One request, host memory, caller-owned.

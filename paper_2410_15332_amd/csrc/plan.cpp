@@ -31,6 +31,9 @@ epic_status validate_attn_cfg(const epic_attn_cfg* cfg) {
     return fail(EPIC_ERR_UNSUPPORTED, "block_size %d not supported (16)", cfg->block_size);
   if (cfg->kv_split_blocks < 0)
     return fail(EPIC_ERR_INVALID_ARG, "kv_split_blocks %d < 0", cfg->kv_split_blocks);
+  if (cfg->tile_rows != 0 && !valid_tile_rows(cfg->tile_rows))
+    return fail(EPIC_ERR_UNSUPPORTED, "tile_rows %d (expected 0, %d or %d)", cfg->tile_rows, kTileRowsSmall,
+                kTileRowsLarge);
   if (!(cfg->softmax_scale >= 0.0f)) return fail(EPIC_ERR_INVALID_ARG, "softmax_scale must be >= 0");
   return EPIC_OK;
 }
@@ -280,8 +283,10 @@ epic_status plan_shape(const epic_link_request* reqs, int32_t batch, const epic_
   int split = split_blocks(cfg, large, kShapeLarge, &est);
   int64_t large_items = 0;
   for (const Tile& t : large) large_items += std::max(1, cdiv(t.nblk, split));
-  const bool use_large = row_steps(large, kTileRowsLarge) * 100 <= row_steps(small, kTileRowsSmall) * 101 &&
-                         large_items * cfg->num_kv_heads >= kShapeLarge.slots;
+  const bool use_large = cfg->tile_rows != 0
+                             ? cfg->tile_rows == kTileRowsLarge
+                             : row_steps(large, kTileRowsLarge) * 100 <= row_steps(small, kTileRowsSmall) * 101 &&
+                                   large_items * cfg->num_kv_heads >= kShapeLarge.slots;
   if (use_large) {
     tiles.swap(large);
     s.tile_rows = kTileRowsLarge;

@@ -47,7 +47,8 @@ _i32p = C.POINTER(C.c_int32)
 
 class epic_attn_cfg(C.Structure):
     _fields_ = [("num_q_heads", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32),
-                ("block_size", C.c_int32), ("softmax_scale", C.c_float), ("kv_split_blocks", C.c_int32)]
+                ("block_size", C.c_int32), ("softmax_scale", C.c_float), ("kv_split_blocks", C.c_int32),
+                ("tile_rows", C.c_int32)]
 
 
 class epic_link_request(C.Structure):
@@ -141,8 +142,8 @@ class Request:
     k: int
 
 
-def attn_cfg(hq: int, hkv: int, d: int, scale: float = 0.0, split_blocks: int = 0) -> epic_attn_cfg:
-    return epic_attn_cfg(hq, hkv, d, BLOCK, scale, split_blocks)
+def attn_cfg(hq: int, hkv: int, d: int, scale: float = 0.0, split_blocks: int = 0, tile_rows: int = 0) -> epic_attn_cfg:
+    return epic_attn_cfg(hq, hkv, d, BLOCK, scale, split_blocks, tile_rows)
 
 
 class _ReqArray:

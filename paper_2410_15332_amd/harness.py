@@ -60,13 +60,13 @@ def chunk_ids(wl: AttnWorkload) -> List[int]:
 
 
 def stage_attention(wl: AttnWorkload, device="cuda", split_blocks: int = 0, spare_blocks: int = 0,
-                    threads: int = 8) -> AttnStage:
+                    threads: int = 8, tile_rows: int = 0) -> AttnStage:
     """Chunk pool + plan + S-row inputs + output buffers for an attention-level workload."""
     import torch
     from concurrent.futures import ThreadPoolExecutor
 
     hq, hkv, d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
-    cfg = el.attn_cfg(hq, hkv, d, 0.0, split_blocks)
+    cfg = el.attn_cfg(hq, hkv, d, 0.0, split_blocks, tile_rows)
     ids = chunk_ids(wl)
     nb = {c: -(-wl.chunk_lens[c] // el.BLOCK) for c in ids}
     n_chunk_blocks = sum(nb.values())

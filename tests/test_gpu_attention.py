@@ -165,19 +165,27 @@ EDGE = [
 ]
 
 
+# 128-row tiles run the 4-wavefront kernel (two buffers per operand), 256-row
+# tiles the 8-wavefront kernel (three buffers, loads two steps ahead)
+TILE_ROWS = [128, 256]
+
+
+@pytest.mark.parametrize("tile_rows", TILE_ROWS)
 @pytest.mark.parametrize("wl", EDGE, ids=[w.name for w in EDGE])
-def test_edge_cases(wl):
-    st = _stage(wl)
+def test_edge_cases(wl, tile_rows):
+    st = _stage(wl, tile_rows=tile_rows)
+    assert st.sizes.tile_rows == tile_rows
     st.run()
     check_stage(st)
 
 
+@pytest.mark.parametrize("tile_rows", TILE_ROWS)
 @pytest.mark.parametrize("split", [4, 8, 36])
-def test_forced_split_kv(split):
+def test_forced_split_kv(split, tile_rows):
     """Small split sizes: most rows merge many partials in the combine kernel."""
     wl = _wl("split", [300, 211, 129], [[0, 1, 2]], [70], 24, 32, 8, 128)
-    st = _stage(wl, split_blocks=split)
-    assert st.sizes.n_partials > 0
+    st = _stage(wl, split_blocks=split, tile_rows=tile_rows)
+    assert st.sizes.n_partials > 0 and st.sizes.tile_rows == tile_rows
     st.run()
     check_stage(st)
 
@@ -192,10 +200,11 @@ def test_empty_selection_launches_nothing():
     assert np.array_equal(before, _bits(st.k_cache))
 
 
-def test_deterministic():
+@pytest.mark.parametrize("tile_rows", TILE_ROWS)
+def test_deterministic(tile_rows):
     """Two runs give bit-identical outputs (cheap check for races in write/combine)."""
     wl = _wl("det", [300, 211, 129], [[0, 1, 2]], [70], 24, 32, 8, 128)
-    st = _stage(wl, split_blocks=8)
+    st = _stage(wl, split_blocks=8, tile_rows=tile_rows)
     st.run()
     o1, l1 = st.out.clone(), st.lse.clone()
     st.run()

@@ -22,8 +22,8 @@ def _random_requests(rng, batch, max_chunks=6, max_len=70, pool=None):
     return reqs, nxt
 
 
-def _plan(reqs, n_used, hq=8, hkv=2, d=128, split=0, extra=3):
-    cfg = el.attn_cfg(hq, hkv, d, 0.0, split)
+def _plan(reqs, n_used, hq=8, hkv=2, d=128, split=0, extra=3, tile_rows=0):
+    cfg = el.attn_cfg(hq, hkv, d, 0.0, split, tile_rows)
     need = el.epic_plan_sizes_get(reqs, cfg, 1 << 30).n_private
     free = list(range(n_used, n_used + need + extra))
     sizes, buf, v = el.epic_plan_link(reqs, cfg, free, n_used + need + extra)
@@ -93,11 +93,13 @@ def test_cow_sources():
         assert v["priv_src"].tolist() == srcs
 
 
-def test_work_items_cover_causal_ranges():
+@pytest.mark.parametrize("tile_rows", [0, 128, 256])
+def test_work_items_cover_causal_ranges(tile_rows):
     rng = np.random.default_rng(9)
     reqs, n_used = _random_requests(rng, 3, max_chunks=8, max_len=300)
     for split in (0, 4, 16):
-        cfg, sizes, v, _ = _plan(reqs, n_used, 32, 8, split=split)
+        cfg, sizes, v, _ = _plan(reqs, n_used, 32, 8, split=split, tile_rows=tile_rows)
+        assert sizes.tile_rows in ((128, 256) if tile_rows == 0 else (tile_rows,))
         R = sizes.tile_rows // 4
         tiles = v["tiles"].reshape(-1, 4)
         work = v["work"].reshape(-1, el.WORK_INTS)
@@ -185,3 +187,35 @@ def test_repeated_chunk_in_request():
     sizes, _, v = el.epic_plan_link(reqs, cfg, [2, 3], 4)
     assert v["linked_blocks"].tolist() == [0, 1, 2, 1, 3]
     assert v["priv_src"].tolist() == [0, -1]
+
+
+def _long_request(lens, suffix, k):
+    blocks, nxt = [], 0
+    for L in lens:
+        nb = -(-L // 16)
+        blocks.append(list(range(nxt, nxt + nb)))
+        nxt += nb
+    return [el.Request(lens, blocks, suffix, k)], nxt
+
+
+@pytest.mark.parametrize("lens,suffix,k,want", [
+    ([2048] * 16, 256, -1, 256),   # recompute-all: every tile is one stretch of positions
+    ([2048] * 64, 256, 0, 256),    # suffix only (Naive), split until every CU has a workgroup
+    ([2048] * 64, 256, 32, 128),   # first 32 rows of each chunk: 256-row tiles span two chunks
+    ([512] * 10, 64, 16, 128),     # small: 256-row tiles would leave CUs idle
+])
+def test_tile_rows_default(lens, suffix, k, want):
+    """256-row tiles only when their rows need nearly the same keys and the launch fills the chip."""
+    reqs, n = _long_request(lens, suffix, k)
+    cfg, sizes, v, _ = _plan(reqs, n, 32, 8)
+    assert sizes.tile_rows == want
+
+
+def test_tile_rows_override_and_rejection():
+    reqs, n = _long_request([300, 211], 40, 16)
+    for tr in (128, 256):
+        _, sizes, _, _ = _plan(reqs, n, 32, 8, tile_rows=tr)
+        assert sizes.tile_rows == tr
+    with pytest.raises(el.EpicError) as e:
+        el.epic_plan_sizes_get(reqs, el.attn_cfg(32, 8, 128, 0.0, 0, 192), 1 << 30)
+    assert e.value.status == 2
