@@ -216,7 +216,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5k32", choices=sorted(WORKLOADS))
     ap.add_argument("--split-blocks", type=int, default=0, help="override the planner's split-KV size")
-    ap.add_argument("--cpu-rows", type=int, default=192, help="S rows in the CPU-oracle sample")
+    ap.add_argument("--cpu-rows", type=int, default=640, help="S rows in the CPU-oracle sample (about 12 s on 16 cores)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="before the timed region, run one device copy of this many MiB (counter calibration)")
@@ -224,7 +224,7 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the link step is built and timed on a single MI355X; "
-              "multi-GPU sharding is described in DESIGN.md but not built. Run with --gpus 1.", file=sys.stderr)
+              "the link step runs on one GPU; sharding across GPUs is not built. Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -320,7 +320,7 @@ def main():
                       "combine": round(comb_ms, 5)},
         "roofline": {
             "bound": "mfma",
-            "kernel": "link_attention_kernel<128>",
+            "kernel": f"link_attention_kernel<{wl.head_dim}, {st.sizes.tile_rows // 32}>",
             "achieved": round(achieved, 2),
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",

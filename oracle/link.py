@@ -2,10 +2,10 @@
 
 Notation follows Sec. 4.2: the k' selected tokens are recomputed, K_exp / V_exp
 (N rows) hold the cached KV of the N - k' unselected tokens plus the
-recomputed rows "at correct positions", and A = softmax(Q K_exp^T . MASK) with
+recomputed rows, each at its own linked position, and A = softmax(Q K_exp^T . MASK) with
 MASK letting each selected token attend only to tokens at or before it.
 
-Readings where the paper is silent (each one is a choice, listed in the design doc):
+Readings where the paper is silent (each one is a choice):
   * the logits are scaled by 1/sqrt(d) (standard attention; needed for
     recompute-everything to equal an ordinary prefill);
   * MASK is additive -inf (a masked key gets zero weight), and a token attends

@@ -1,7 +1,7 @@
 // Link write: build every request-private block of the linked cache.
 //
 // Sec. 4.2 forms K_exp / V_exp from the cached vectors of the unselected tokens
-// plus the recomputed vectors "at correct positions".  Shared chunk blocks are
+// plus the recomputed vectors, each at its own linked position.  Shared chunk blocks are
 // immutable, so a block that receives a recomputed row is private: its cached
 // rows are copied from the shared block (copy-on-write) and its selected rows
 // take k_s / v_s.  Each private block is written exactly once, by one

@@ -158,8 +158,8 @@ struct TileShape {
   int rows, slots;
   double step_cost, item_overhead, partial_cost;
 };
-constexpr TileShape kShapeLarge{kTileRowsLarge, 256, 1.0, 3.0, 1.5};   // one 8-wavefront workgroup per CU, 256 CUs
-constexpr TileShape kShapeSmall{kTileRowsSmall, 512, 1.0, 2.0, 1.5};   // two 4-wavefront workgroups per CU
+constexpr TileShape kShapeLarge{kTileRowsLarge, 256, 1.0, 3.0, 4.0};   // one 8-wavefront workgroup per CU, 256 CUs
+constexpr TileShape kShapeSmall{kTileRowsSmall, 512, 1.0, 2.0, 4.0};   // two 4-wavefront workgroups per CU
 
 // Estimated duration of the attention launch for a split: the items (times the
 // KV heads, head-minor as in the grid) are dealt in launch order to the
@@ -187,8 +187,8 @@ double estimate_makespan(const std::vector<Tile>& tiles, int split, int hkv, con
 // Key blocks per split-KV work item: among splits max_nblk / n (n from 1 to 128
 // in about geometric steps, rounded up to whole 4-block tiles, never below 64
 // blocks, because every split writes and re-reads a tile of fp32 partial
-// results), the one with the shortest estimated launch; ties go to the larger
-// split (fewer partials).  *time receives that estimate.
+// results), the one with the shortest estimated launch, where a finer split
+// must be 3% shorter to win (fewer partials).  *time receives that estimate.
 int split_blocks(const epic_attn_cfg* cfg, const std::vector<Tile>& tiles, const TileShape& sh, double* time) {
   const int hkv = cfg->num_kv_heads;
   if (cfg->kv_split_blocks > 0) {
@@ -217,7 +217,7 @@ int split_blocks(const epic_attn_cfg* cfg, const std::vector<Tile>& tiles, const
       prev = split;
       if (n_items(split) * hkv > kMaxRounds * sh.slots) break;
       const double t = estimate_makespan(tiles, split, hkv, sh);
-      if (t < best_time * 0.999) {
+      if (t < best_time * 0.97) {               // finer splits must pay for their partials clearly
         best_time = t;
         best = split;
       }
