@@ -192,8 +192,8 @@ epic_status epic_set_profile_events(void* const* events);
 
 /* Llama-style decoder (Sec. 5.1 models): pre-norm RMSNorm, rotary embedding
  * (pairs (i, i + D/2), inverse frequency theta^(-2i/D), angles in float64),
- * GQA attention, SwiGLU MLP, final RMSNorm.  hidden % 256 == 0 and
- * ffn % 256 == 0 are required. */
+ * GQA attention, SwiGLU MLP, final RMSNorm.  hidden % 128 == 0,
+ * ffn % 128 == 0 and (Hq + 2 Hkv) D % 128 == 0 are required. */
 typedef struct {
   epic_attn_cfg attn;
   int32_t hidden;
@@ -240,6 +240,29 @@ epic_status epic_link_model(const epic_model_cfg* cfg, const epic_layer_weights*
                             float* hidden_s, uint16_t* const* k_caches, uint16_t* const* v_caches,
                             float* out_hidden, void* workspace, size_t workspace_bytes,
                             void* stream);
+
+/* ---------------------------------------------------------------- projections */
+
+/* The projection GEMM that epic_link_layer / epic_link_model run for the S rows
+ * (Sec. 4.2: Q = E W_Q, K = E W_K, V = E W_V of the selected rows, then the output
+ * projection W_O; the model's SwiGLU MLP), on its own:
+ *   C[i][j] = sum_t a[i][t] w[j][t]     a: bf16 [m][k]; w: bf16 [n][k] ([out][in]);
+ *                                       fp32 accumulation
+ * epilogue EPIC_GEMM_STORE:    c[i][j] = C[i][j]                       c: fp32 [m][n]
+ *          EPIC_GEMM_RESIDUAL: c[i][j] += C[i][j]                      c: fp32 [m][n], in place
+ *          EPIC_GEMM_SWIGLU:   act[i][j] = bf16(silu(C[i][j]) C[i][j + n/2]), j < n/2
+ *                              (rows [0, n/2) of w: gate; [n/2, n): up)   act: bf16 [m][n/2]
+ * Shapes: m >= 0, k % 32 == 0, n % 128 == 0, and with m rounded up to a multiple
+ * of 256 every operand and output below 2^31 bytes; else EPIC_ERR_UNSUPPORTED.
+ * Device pointers, 16-byte aligned.  workspace: at least epic_gemm_workspace_bytes()
+ * bytes of device memory, 256-byte aligned, owned by the caller; it holds the
+ * partial sums of output tiles cut along k and their arrival counters (cleared by
+ * this call), so calls in flight at the same time need separate workspaces.
+ * Enqueued on `stream` (NULL: the default stream); returns after the enqueue. */
+typedef enum { EPIC_GEMM_STORE = 0, EPIC_GEMM_RESIDUAL = 1, EPIC_GEMM_SWIGLU = 2 } epic_gemm_epilogue;
+size_t epic_gemm_workspace_bytes(void);
+epic_status epic_gemm(int32_t epilogue, const uint16_t* a, const uint16_t* w, int32_t m, int32_t n, int32_t k,
+                      float* c, uint16_t* act, void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -12,12 +12,14 @@ Contents
   link.py   -- token selection (Sec. 4.2), KV expansion (Sec. 4.2, third step),
                masked attention (Eq. 1), attention-level link step.
   model.py  -- Llama-style decoder layer for the selected rows, the compile step
-               (Sec. 2.2) and the full-model link step.
+               (Sec. 2.2), the full-model link step, and the layer's row-set
+               projections on their own.
 
 Pins (tests/test_oracle_pins.py) tie each function to something other than
 itself: library causal attention (FR = full prefill, Sec. 2.3), the Naive
 special case (k = 0), closed forms (one-hot and constant V, zero queries,
-position 0), a worked selection example, and the HuggingFace Llama forward.
+position 0), a worked selection example, the HuggingFace Llama forward, and
+brute-force sums for the projections.
 """
 from .link import (  # noqa: F401
     chunk_offsets,
@@ -27,6 +29,7 @@ from .link import (  # noqa: F401
     link_attention,
 )
 from .model import (  # noqa: F401
+    projection,
     rmsnorm,
     rope,
     compile_chunk,

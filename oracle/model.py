@@ -61,6 +61,23 @@ def _silu(x: np.ndarray) -> np.ndarray:
     return x / (1.0 + np.exp(-x))
 
 
+def projection(a: np.ndarray, w: np.ndarray, epilogue: str, c_in: np.ndarray = None) -> np.ndarray:
+    """The row-set projections of a layer (Sec. 4.2: Q = E W_Q, ...; O = A V_exp W_O;
+    the model's SwiGLU MLP) as plain definitions on float64 inputs:
+    "store"    a @ w.T
+    "residual" c_in + a @ w.T
+    "swiglu"   silu(g) * u with [g | u] = a @ w.T split in halves (gate rows first)."""
+    y = a @ w.T
+    if epilogue == "store":
+        return y
+    if epilogue == "residual":
+        return c_in + y
+    if epilogue == "swiglu":
+        f = w.shape[0] // 2
+        return _silu(y[:, :f]) * y[:, f:]
+    raise ValueError(epilogue)
+
+
 class _Cfg:
     def __init__(self, hidden, ffn, hq, hkv, d, theta, eps):
         self.hidden, self.ffn, self.hq, self.hkv, self.d = hidden, ffn, hq, hkv, d

@@ -7,190 +7,444 @@
 //   kResidual : h[M][N] += C                         (W_O and W_down; fp32 residual stream)
 //   kSwiGLU   : act[M][N/2] = silu(gate) * up, bf16  (W_gate_up; gate rows [0, F), up rows [F, 2F))
 //
-// Tiling: 256 threads = 4 wavefronts, workgroup tile 128 x 128 (or 128 x 64 for
-// narrow outputs), each wavefront 64 x 64 (64 x 32) as 2 x 2 (2 x 1)
-// v_mfma_f32_32x32x16_bf16 tiles, K in steps of 64 staged in
-// LDS (rows padded to 144 bytes so the 16 rows one ds_read_b128 pass touches
-// fall in distinct banks).  Global loads run two K steps ahead through two
-// register stages, so each load has two steps of MFMA work to arrive.  Tiles
-// are ordered so that the M tiles sharing one weight tile are launched together
-// on one XCD (workgroups are dealt round-robin to the 8 XCDs), which then reads
-// that weight tile from HBM once and from its L2 afterwards.  For kSwiGLU the
-// 128 weight rows of a tile are gate/up in 32-row groups (gate j.., up j..,
-// gate j+32.., up j+32..), so each wavefront's two 32-column MFMA tiles hold
-// gate and up of the same 32 outputs in the same registers.
-// Rows past M are computed from a clamped row and never stored.
+// Tiling: workgroup tile 256 x TN, 8 wavefronts of 64 columns each (TN = 256:
+// 2 x 4 wavefronts of 128 x 64, i.e. 4 x 2 v_mfma_f32_32x32x16_bf16 tiles; TN = 128:
+// 4 x 2 wavefronts of 64 x 64).  K runs in stages of 32 staged in LDS by direct
+// buffer->LDS loads, NS stages in flight (loads issued NS - 1 stages ahead of use).  An operand stage is 16 groups of 16 rows; row r of a group sits at
+// byte 64 r with its four 16-byte chunks XOR-swizzled by (r / 4) % 4, so one load
+// instruction fills one group (1 KB) and the 16 lanes of each ds_read_b128 group
+// touch distinct banks.  For kSwiGLU the TN weight rows of a tile are gate/up in
+// 32-row groups (gate j.., up j.., gate j+32.., ...), so a wavefront's two
+// 32-column MFMA tiles hold gate and up of the same 32 outputs.
+//
+// Scheduling: at most one workgroup per CU (G of them), persistent.  With at least
+// a round of 256 x 256 tiles, whole tiles are dealt in rounds of G, G chosen so the
+// rounds are (nearly) full.  With fewer tiles (short row sets), 256 x 128 tiles are
+// used and the ones that do not fill whole rounds (the last partial round plus one
+// full round, or all of them) are cut along K into G equal shares of K stages, one
+// per workgroup, so every CU gets the same work.
+// A tile cut across workgroups: each writes its fp32 partial, bumps the tile's
+// arrival counter, and the last to arrive sums the partials in K order (the result
+// does not depend on arrival order) and runs the epilogue.  No workgroup waits for
+// another.  Workgroups are dealt round-robin to the 8 XCDs; worker indices are
+// arranged so that each XCD works on a contiguous run of tiles, and tiles are
+// ordered in groups of up to 8 row tiles per weight tile, so concurrent workgroups
+// on an XCD share operands through its L2.
+// Rows past M and columns past N are computed from clamped rows and never stored.
+#include <algorithm>
+
 #include "device_common.h"
-#include "kernels.h"
+#include "gemm.h"
 
 namespace epic {
 
 namespace {
 
-constexpr int kBM = 128, kBK = 64;
-constexpr int kLdsRow = kBK + 8;   // elements per LDS row (144 bytes)
-constexpr int kGemmThreads = 256;
-constexpr int kChunks = kBM * kBK / 8 / kGemmThreads;   // 16-byte A chunks per thread (4)
+constexpr int kTM = 256, kBK = 32;
+constexpr int kThreads = 512;
+constexpr int kBufWord3 = 0x00020000;                   // gfx9 raw buffer descriptor word 3
+constexpr int kMaxWorkers = 256;                        // one workgroup per CU
+constexpr int kPartialFloats = kTM * 256;               // fp32 partial sums of the largest tile
+constexpr int kMaxSplitTiles = 2 * kMaxWorkers;
+constexpr int kMinUnits = 8;                            // K stages per workgroup, at least
 
-// kBN = 128 (wavefront tile 64 x 64) or 64 (64 x 32, for narrow outputs whose
-// 128-wide tiles would leave CUs idle).
-template <int EPI, int kBN>
-__global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
-  constexpr int NJ = kBN / 64;                          // 32-column MFMA tiles per wavefront
-  constexpr int kBChunks = kBN * kBK / 8 / kGemmThreads; // 16-byte B chunks per thread
-  __shared__ __attribute__((aligned(16))) uint16_t lds_a[2][kBM * kLdsRow];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_b[2][kBN * kLdsRow];
+template <int TN>
+struct Shape {
+  static constexpr int NS = TN == 256 ? 4 : 6;          // LDS stages
+  static constexpr int WAVES_M = TN == 256 ? 2 : 4;     // wavefronts along M
+  static constexpr int WM = kTM / WAVES_M;              // rows per wavefront
+  static constexpr int I = WM / 32;                     // 32-row MFMA tiles per wavefront
+  static constexpr int J = 2;                           // 32-column MFMA tiles per wavefront
+  static constexpr int A_STAGE = kTM * kBK * 2;         // bytes per stage
+  static constexpr int B_STAGE = TN * kBK * 2;
+  static constexpr int NLB = TN / 64;                   // W row groups per loading wavefront
+};
 
-  const int m_tiles = (g.M + kBM - 1) / kBM;
-  const int n_tiles = EPI == kSwiGLU ? g.ffn / 64 : g.N / kBN;
-  const int total = m_tiles * n_tiles;
-  int tile_id = blockIdx.x;
-  if (total % 8 == 0) tile_id = (blockIdx.x % 8) * (total / 8) + blockIdx.x / 8;   // XCD-contiguous ranges
-  const int mt = tile_id % m_tiles;
-  const int nt = tile_id / m_tiles;
-  const int m0 = mt * kBM;
-  const int tid = threadIdx.x & (kGemmThreads - 1);
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int col = lane & 31, half = lane >> 5;
+struct GemmPlan {
+  int m_tiles, n_tiles, ks;    // tiles along M and N, K stages per tile
+  int gm;                      // row tiles per ordering group
+  int G;                       // workgroups
+  int dp_rounds, dp_tiles;     // whole-tile rounds and the tiles they cover (tiles 0 .. dp_tiles-1)
+  int sk_units;                // K stages of the cut tiles (tiles dp_tiles ..)
+};
 
-  // weight row of tile column c
-  auto wrow = [&](int c) -> int {
-    if constexpr (EPI == kSwiGLU) {
-      const int grp = c >> 5;                // 0: gate, 1: up, 2: gate, 3: up
-      return (grp & 1) * g.ffn + nt * 64 + (grp >> 1) * 32 + (c & 31);
+template <int TN>
+struct GemmLds {
+  char a[Shape<TN>::NS][Shape<TN>::A_STAGE];
+  char b[Shape<TN>::NS][Shape<TN>::B_STAGE];
+  int flag;
+};
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Workgroup barrier ordering LDS accesses only (waits for this wavefront's LDS
+// reads, not for its buffer->LDS loads still in flight).
+__device__ __forceinline__ void barrier_lds() {
+  __asm__ volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+// At most N of this wavefront's vector memory operations outstanding (they
+// complete in issue order); gfx9 encoding: vmcnt bits [3:0] and [15:14].
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+}
+
+// Position in a workgroup's sequence of K stages: tile, stage, and the stage range
+// [kbeg, kend) of the current segment (the part of the tile this workgroup owns).
+struct Cursor {
+  int u, tile, kt, kbeg, kend;
+};
+
+template <int EPI, int TN>
+__global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan p) {
+  using SH = Shape<TN>;
+  constexpr int NS = SH::NS, I = SH::I, J = SH::J;
+  __shared__ __attribute__((aligned(1024))) GemmLds<TN> lds;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wv % SH::WAVES_M, wn = wv / SH::WAVES_M;   // wavefront tile: rows wm*WM.., columns wn*64..
+  const int w = blockIdx.x;
+  const int wr = p.G % 8 == 0 ? (w % 8) * (p.G / 8) + w / 8 : w;   // XCD-contiguous worker index
+  const int64_t su = p.sk_units;
+  const int s0 = int(int64_t(wr) * su / p.G), s1 = int(int64_t(wr + 1) * su / p.G);
+  // whole tiles wr, wr + G, .. below dp_tiles (the last round may be short), then the K share
+  const int dp_units = (wr < p.dp_tiles ? (p.dp_tiles - wr + p.G - 1) / p.G : 0) * p.ks;
+  const int n_units = dp_units + (s1 - s0);
+  if (n_units == 0) return;             // (no such workgroup is launched; kept as a guard)
+
+  auto tile_mn = [&](int t, int& mt, int& nt) __attribute__((always_inline)) {
+    const int per_group = p.gm * p.n_tiles;
+    const int grp = t / per_group;
+    const int first = grp * p.gm;
+    const int gsz = min(p.m_tiles - first, p.gm);
+    const int r = t - grp * per_group;
+    mt = first + r % gsz;
+    nt = r / gsz;
+  };
+  auto seek = [&](Cursor& c, int u) __attribute__((always_inline)) {   // u: first unit of a segment
+    c.u = u;
+    if (u < dp_units) {
+      c.tile = (u / p.ks) * p.G + wr;
+      c.kbeg = 0;
+      c.kend = p.ks;
     } else {
-      return nt * kBN + c;
+      const int v = s0 + (u - dp_units);
+      const int q = v / p.ks;
+      c.tile = p.dp_tiles + q;
+      c.kbeg = v - q * p.ks;
+      c.kend = min(p.ks, s1 - q * p.ks);
     }
+    c.kt = c.kbeg;
+  };
+  auto advance = [&](Cursor& c) __attribute__((always_inline)) {      // to the next unit; stays on the last one
+    if (c.u + 1 >= n_units) return;
+    ++c.u;
+    if (++c.kt == c.kend) seek(c, c.u);
   };
 
-  // global -> register staging: chunk i of a thread = row ld_row + 32 i, 8 k at ld_kc
-  const int ld_row = tid >> 3, ld_kc = (tid & 7) * 8;
-  const uint16_t* a_ptr[kChunks];
-  const uint16_t* b_ptr[kBChunks];
+  // ---- buffer->LDS loads: wavefronts 0..3 stage the 16 A row groups (4 each),
+  // 4..7 the TN / 16 W row groups (NLB each).
+  const bool a_wave = wv < 4;
+  const int nl = a_wave ? 4 : SH::NLB;                     // loads per stage of this wavefront
+  const int grp0 = nl * (wv & 3);
+  const int lrow = lane >> 2;                              // row within a 16-row group
+  const int lchunk = (lane & 3) ^ ((lane >> 4) & 3);       // 16-byte chunk of that row this lane loads
+  const int row_bytes = g.K * 2;
+  const int w_rows = EPI == kSwiGLU ? 2 * g.ffn : g.N;
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a_wave ? g.A : g.W), 0, (a_wave ? g.M : w_rows) * row_bytes, kBufWord3);
+  int vo[4];                                               // lane byte offsets of the row groups
+  auto dma_setup = [&](int tile) __attribute__((always_inline)) {
+    int mt, nt;
+    tile_mn(tile, mt, nt);
 #pragma unroll
-  for (int i = 0; i < kChunks; ++i) a_ptr[i] = g.A + size_t(min(m0 + ld_row + 32 * i, g.M - 1)) * g.K + ld_kc;
-#pragma unroll
-  for (int i = 0; i < kBChunks; ++i) b_ptr[i] = g.W + size_t(wrow(ld_row + 32 * i)) * g.K + ld_kc;
-  typedef uint32_t stage_t __attribute__((ext_vector_type(4 * (kChunks + kBChunks))));   // A then B chunks
-  stage_t st0, st1;
-  auto load = [&](int kt, stage_t& st) {
-#pragma unroll
-    for (int i = 0; i < kChunks; ++i) {
-      const uint4 a = *reinterpret_cast<const uint4*>(a_ptr[i] + kt * kBK);
-      st[4 * i + 0] = a.x; st[4 * i + 1] = a.y; st[4 * i + 2] = a.z; st[4 * i + 3] = a.w;
-    }
-#pragma unroll
-    for (int i = 0; i < kBChunks; ++i) {
-      const uint4 b = *reinterpret_cast<const uint4*>(b_ptr[i] + kt * kBK);
-      st[4 * kChunks + 4 * i + 0] = b.x; st[4 * kChunks + 4 * i + 1] = b.y;
-      st[4 * kChunks + 4 * i + 2] = b.z; st[4 * kChunks + 4 * i + 3] = b.w;
-    }
-  };
-  auto store = [&](int buf, const stage_t& st) {
-#pragma unroll
-    for (int i = 0; i < kChunks; ++i)
-      *reinterpret_cast<uint4*>(&lds_a[buf][(ld_row + 32 * i) * kLdsRow + ld_kc]) =
-          make_uint4(st[4 * i + 0], st[4 * i + 1], st[4 * i + 2], st[4 * i + 3]);
-#pragma unroll
-    for (int i = 0; i < kBChunks; ++i)
-      *reinterpret_cast<uint4*>(&lds_b[buf][(ld_row + 32 * i) * kLdsRow + ld_kc]) =
-          make_uint4(st[4 * kChunks + 4 * i + 0], st[4 * kChunks + 4 * i + 1], st[4 * kChunks + 4 * i + 2],
-                     st[4 * kChunks + 4 * i + 3]);
-  };
-
-  f32x16 acc[2][NJ];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x16{};
-
-  auto compute = [&](int buf) {
-#pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
-      bf16x8 af[2], bfr[NJ];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(&lds_a[buf][(wm * 64 + i * 32 + col) * kLdsRow + ks * 16 + half * 8]);
-#pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(
-            &lds_b[buf][(wn * (kBN / 2) + j * 32 + col) * kLdsRow + ks * 16 + half * 8]);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) acc[i][j] = mfma_32x32x16(af[i], bfr[j], acc[i][j]);
+    for (int i = 0; i < 4; ++i) {
+      const int row = (grp0 + i) * 16 + lrow;              // row of the operand tile
+      int gr;
+      if (a_wave) gr = min(mt * kTM + row, g.M - 1);
+      else if constexpr (EPI == kSwiGLU)
+        gr = ((row >> 5) & 1) * g.ffn + nt * (TN / 2) + (row >> 6) * 32 + (row & 31);
+      else gr = min(nt * TN + row, g.N - 1);
+      vo[i] = gr * row_bytes + lchunk * 16;
     }
   };
+  char* const dma_base = a_wave ? lds.a[0] + grp0 * 1024 : lds.b[0] + grp0 * 1024;
+  const int dma_stage = a_wave ? SH::A_STAGE : SH::B_STAGE;
+  auto dma = [&](int buf, int kt) __attribute__((always_inline)) {
+    char* dst = dma_base + buf * dma_stage;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (i < SH::NLB || a_wave)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + i * 1024), 16, vo[i], kt * (kBK * 2), 0, 0);
+  };
 
-  // Pipeline: LDS buffer kt % 2 holds step kt; registers carry steps kt + 1 and kt + 2.
-  const int nk = g.K / kBK;
-  load(0, st0);
-  store(0, st0);
-  if (nk > 1) load(1, st0);
-  if (nk > 2) load(2, st1);
-  __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    compute(0);                                // step kt
-    if (kt + 1 < nk) {
-      store(1, st0);                           // step kt + 1
-      if (kt + 3 < nk) load(kt + 3, st0);
-    }
-    __syncthreads();
-    if (kt + 1 >= nk) break;
-    compute(1);                                // step kt + 1
-    if (kt + 2 < nk) {
-      store(0, st1);                           // step kt + 2
-      if (kt + 4 < nk) load(kt + 4, st1);
-    }
-    __syncthreads();
-  }
+  // ---- MFMA operands: lane l reads row l % 32 of a 32-row tile, 16-byte chunk
+  // 2 ks + l / 32 of the stage, stored at chunk position chunk ^ ((l % 16) / 4).
+  const int lrow16 = ((lane >> 4) & 1) * 1024 + (lane & 15) * 64;
+  const int lb0 = lrow16 + (((lane >> 5) ^ ((lane >> 2) & 3)) * 16);
+  const int lb1 = lrow16 + (((2 + (lane >> 5)) ^ ((lane >> 2) & 3)) * 16);
+  const char* const pa0 = lds.a[0] + wm * (SH::WM / 16) * 1024 + lb0;
+  const char* const pa1 = lds.a[0] + wm * (SH::WM / 16) * 1024 + lb1;
+  const char* const pb0 = lds.b[0] + wn * 4096 + lb0;
+  const char* const pb1 = lds.b[0] + wn * 4096 + lb1;
+  struct Frags {
+    bf16x8 a[I], b[J];
+  };
+  auto read = [&](Frags& f, int buf, int ks) __attribute__((always_inline)) {
+    const char* pa = (ks ? pa1 : pa0) + buf * SH::A_STAGE;
+    const char* pb = (ks ? pb1 : pb0) + buf * SH::B_STAGE;
+#pragma unroll
+    for (int i = 0; i < I; ++i) f.a[i] = *reinterpret_cast<const bf16x8*>(pa + i * 2048);
+#pragma unroll
+    for (int j = 0; j < J; ++j) f.b[j] = *reinterpret_cast<const bf16x8*>(pb + j * 2048);
+  };
 
-  // Epilogue.  acc[i][j] register r: row wm*64 + i*32 + (r/4)*8 + half*4 + r%4,
-  // column wn*(kBN/2) + j*32 + col.
+  f32x16 acc[I][J];
+  auto zero_acc = [&]() __attribute__((always_inline)) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < I; ++i)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = m0 + wm * 64 + i * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-      if (m >= g.M) continue;
-      if constexpr (EPI == kSwiGLU) {
-        const float gt = acc[i][0][r], up = acc[i][1][r];
-        const float act = gt / (1.0f + __expf(-gt)) * up;
-        const int n = nt * 64 + wn * 32 + col;
-        g.act[size_t(m) * g.ffn + n] = uint16_t(pack_bf16x2(act, 0.0f) & 0xFFFFu);
-      } else {
+      for (int j = 0; j < J; ++j) acc[i][j] = f32x16{};
+  };
+  auto mma = [&](const Frags& f) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-          const int n = nt * kBN + wn * (kBN / 2) + j * 32 + col;
-          if constexpr (EPI == kStoreF32)
-            g.C[size_t(m) * g.N + n] = acc[i][j][r];
-          else
-            g.C[size_t(m) * g.N + n] += acc[i][j][r];
+    for (int i = 0; i < I; ++i)
+#pragma unroll
+      for (int j = 0; j < J; ++j) acc[i][j] = mfma_32x32x16(f.a[i], f.b[j], acc[i][j]);
+  };
+
+  // ---- epilogue through buffer descriptors: rows past M fall outside the
+  // descriptor's range (loads read 0, stores are dropped).  Accumulator tile
+  // t = i*J + j, register r: row wm*WM + i*32 + (r/4)*8 + half*4 + r%4, column
+  // wn*64 + j*32 + col of the workgroup tile.  Written CT tiles (CT / J row blocks)
+  // at a time, so the fixup below never holds more than CT tiles of sums.
+  constexpr int CT = 2, NT = I * J, NCH = NT / CT;
+  const int col = lane & 31, half = lane >> 5;
+  auto epilogue_part = [&](int mt, int nt, int h, const f32x16 (&v)[CT]) __attribute__((always_inline)) {
+    const int m0 = mt * kTM + wm * SH::WM + half * 4;
+    if constexpr (EPI == kSwiGLU) {
+      const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(g.act, 0, g.M * g.ffn * 2, kBufWord3);
+      const int n = nt * (TN / 2) + wn * 32 + col;
+#pragma unroll
+      for (int ii = 0; ii < CT / J; ++ii)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + (h * (CT / J) + ii) * 32 + (r >> 2) * 8 + (r & 3);
+          const float gt = v[ii * J + 0][r], up = v[ii * J + 1][r];
+          const float act = gt * __builtin_amdgcn_rcpf(1.0f + fast_exp2(-gt * kLog2e)) * up;
+          __builtin_amdgcn_raw_buffer_store_b16(uint16_t(pack_bf16x2(act, 0.0f) & 0xFFFFu), ro, (m * g.ffn + n) * 2,
+                                                0, 0);
         }
-      }
+    } else {
+      if (nt * TN + wn * 64 >= g.N) return;                // this wavefront's columns are past N
+      const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(g.C, 0, g.M * g.N * 4, kBufWord3);
+      const int n = nt * TN + wn * 64 + col;
+#pragma unroll
+      for (int ii = 0; ii < CT / J; ++ii)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + (h * (CT / J) + ii) * 32 + (r >> 2) * 8 + (r & 3);
+#pragma unroll
+          for (int j = 0; j < J; ++j) {
+            const int off = (m * g.N + n + j * 32) * 4;
+            float x = v[ii * J + j][r];
+            if constexpr (EPI == kResidual)
+              x += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ro, off, 0, 0));
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), ro, off, 0, 0);
+          }
+        }
     }
+  };
+
+  // End of a segment: a whole tile goes straight to the epilogue; a cut tile
+  // through the partial buffers and its arrival counter.
+  constexpr int kWaveFloats = NT * 16 * 64;
+  auto finish = [&](const Cursor& c) __attribute__((always_inline)) {
+    int mt, nt;
+    tile_mn(c.tile, mt, nt);
+    if (c.kbeg == 0 && c.kend == p.ks) {
+#pragma unroll
+      for (int h = 0; h < NCH; ++h) {
+        f32x16 v[CT];
+#pragma unroll
+        for (int t = 0; t < CT; ++t) v[t] = acc[(h * CT + t) / J][(h * CT + t) % J];
+        epilogue_part(mt, nt, h, v);
+      }
+      return;
+    }
+    const int q = c.tile - p.dp_tiles;
+    const int64_t U = p.sk_units;
+    auto owner = [&](int64_t v) __attribute__((always_inline)) { return int(((v + 1) * p.G + U - 1) / U - 1); };
+    const int wf = owner(int64_t(q) * p.ks), wl = owner(int64_t(q + 1) * p.ks - 1);
+    // worker x's partial of this tile (this wavefront's part): its last segment if
+    // it owns the tile's first stage (slot 2x + 1), else its first segment (slot 2x).
+    // Layout: [wavefront][tile t][register quad][lane][4] floats, so each access is
+    // 16 bytes per lane, 1 KB per instruction.  Partials are written and read with
+    // device-coherent accesses (sc1), which go past the XCD's L2, so no cache-wide
+    // write-back or invalidate is needed.
+    const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+        g.partial, 0, 2 * kMaxWorkers * kPartialFloats * 4, kBufWord3);
+    auto slot_off = [&](int x) __attribute__((always_inline)) {   // bytes
+      return int((2 * x + (x == wf ? 1 : 0)) * kPartialFloats + wv * kWaveFloats) * 4 + lane * 16;
+    };
+    constexpr int kSc1 = 16;             // cache policy: system coherent
+    typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+    const int mine = slot_off(wr);
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const f32x16& a16 = acc[t / J][t % J];
+        const f32x4 v4 = {a16[4 * qd], a16[4 * qd + 1], a16[4 * qd + 2], a16[4 * qd + 3]};
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4v, v4), rp, mine + (t * 4 + qd) * 1024, 0,
+                                               kSc1);
+      }
+    wait_vmem<0>();                      // this wavefront's partial has landed ...
+    barrier_lds();                       // ... and every wavefront's, before the count
+    if (tid == 0) lds.flag = atomicAdd(&g.tile_count[q], 1);
+    barrier_lds();
+    const int before = lds.flag;
+    if (before != wl - wf) return;       // not the last to arrive
+#pragma unroll
+    for (int h = 0; h < NCH; ++h) {      // sum the partials in K order, CT tiles at a time
+      f32x16 v[CT];
+#pragma unroll
+      for (int t = 0; t < CT; ++t) v[t] = f32x16{};
+      for (int x = wf; x <= wl; ++x) {
+        const int off = slot_off(x);
+#pragma unroll
+        for (int t = 0; t < CT; ++t)
+#pragma unroll
+          for (int qd = 0; qd < 4; ++qd) {
+            const f32x4 p4 = __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off + ((h * CT + t) * 4 + qd) * 1024, 0, kSc1));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[t][4 * qd + e] += p4[e];
+          }
+      }
+      epilogue_part(mt, nt, h, v);
+    }
+    if (tid == 0) atomicExch(&g.tile_count[q], 0);   // ready for the next launch
+  };
+
+  // ---- pipeline: unit u (one K stage of one tile) lives in LDS buffer u % NS.
+  // Step u reads its second k-slice while the first runs on the matrix cores,
+  // waits for this wavefront's loads of unit u + 1, and after the barrier (all
+  // loads of u + 1 visible, every read of buffer u % NS done) refills that buffer
+  // with unit u + NS and reads the first k-slice of u + 1.  Loads past the last
+  // unit repeat it, so every step leaves the same number in flight.
+  Cursor cc, dc;
+  seek(cc, 0);
+  dc = cc;
+  int dtile = dc.tile;
+  dma_setup(dtile);
+  auto dma_next = [&](int buf) __attribute__((always_inline)) {
+    dma(buf, dc.kt);
+    advance(dc);
+    if (dc.tile != dtile) {
+      dtile = dc.tile;
+      dma_setup(dtile);
+    }
+  };
+#pragma unroll
+  for (int b = 0; b < NS; ++b) dma_next(b);
+  if (a_wave) wait_vmem<(NS - 1) * 4>();            // unit 0 of this wavefront
+  else wait_vmem<(NS - 1) * SH::NLB>();
+  barrier_lds();                                    // ... of every wavefront
+  Frags f0, f1;
+  read(f0, 0, 0);
+  zero_acc();
+  int u = 0, buf = 0;
+  while (true) {
+    // the units of one segment (the epilogue stays out of the hot loop)
+    for (const int ue = u + (cc.kend - cc.kt); u < ue; ++u) {
+      const int nbuf = buf + 1 == NS ? 0 : buf + 1;
+      read(f1, buf, 1);
+      mma(f0);
+      if (a_wave) wait_vmem<(NS - 2) * 4>();        // this wavefront's loads of unit u + 1
+      else wait_vmem<(NS - 2) * SH::NLB>();
+      barrier_lds();
+      dma_next(buf);
+      read(f0, nbuf, 0);
+      mma(f1);
+      buf = nbuf;
+    }
+    finish(cc);
+    if (u >= n_units) break;
+    zero_acc();
+    seek(cc, u);
+  }
+  wait_vmem<0>();                       // no load may land in LDS after the workgroup ends
+}
+
+__global__ void gemm_clear_kernel(int* cnt) {
+  for (int i = threadIdx.x; i < kMaxSplitTiles; i += blockDim.x) cnt[i] = 0;
+}
+
+int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+template <int EPI, int TN>
+void launch_tn(const GemmArgs& g, bool whole_tiles, hipStream_t stream) {
+  GemmPlan p{};
+  p.m_tiles = cdiv(g.M, kTM);
+  p.n_tiles = EPI == kSwiGLU ? g.ffn / (TN / 2) : cdiv(g.N, TN);
+  p.ks = g.K / kBK;
+  p.gm = p.m_tiles < 8 ? p.m_tiles : 8;
+  const int64_t tiles = int64_t(p.m_tiles) * p.n_tiles;
+  if (whole_tiles) {
+    // rounds of whole tiles, as few workgroups as keep the rounds full
+    const int64_t rounds = (tiles + kMaxWorkers - 1) / kMaxWorkers;
+    p.G = int((tiles + rounds - 1) / rounds);
+    p.dp_rounds = int(rounds);
+    p.dp_tiles = int(tiles);                         // a short last round leaves some workgroups idle
+    p.sk_units = 0;
+  } else {
+    const int64_t units = tiles * p.ks;
+    p.G = int(std::min<int64_t>(kMaxWorkers, std::max<int64_t>(1, units / kMinUnits)));
+    const int64_t full = tiles / p.G, rem = tiles % p.G;
+    p.dp_rounds = int(rem == 0 ? full : std::max<int64_t>(full - 1, 0));
+    p.dp_tiles = p.dp_rounds * p.G;
+    p.sk_units = int((tiles - p.dp_tiles) * p.ks);
+  }
+  gemm_kernel<EPI, TN><<<dim3(p.G), kThreads, 0, stream>>>(g, p);
+}
+
+template <int EPI>
+void launch_epi(const GemmArgs& g, hipStream_t stream) {
+  // At least a round of 256 x 256 tiles: whole tiles only (measured: cutting tiles
+  // along K costs about one tile time in partial traffic, more than a short last
+  // round).  Fewer: 256 x 128 tiles, cut along K so that every CU gets a share.
+  const int m_tiles = cdiv(g.M, kTM);
+  const int n256 = EPI == kSwiGLU ? (g.ffn % 128 == 0 ? g.ffn / 128 : 0) : cdiv(g.N, 256);
+  if (int64_t(m_tiles) * n256 >= kMaxWorkers) return launch_tn<EPI, 256>(g, true, stream);
+  launch_tn<EPI, 128>(g, false, stream);
 }
 
 }  // namespace
 
+size_t gemm_workspace_bytes() {
+  return size_t(2 * kMaxWorkers) * kPartialFloats * sizeof(float) + kMaxSplitTiles * sizeof(int);
+}
+
+void gemm_workspace(void* base, float** partial, int** tile_count) {
+  *partial = static_cast<float*>(base);
+  *tile_count = reinterpret_cast<int*>(static_cast<char*>(base) + size_t(2 * kMaxWorkers) * kPartialFloats * 4);
+}
+
+void launch_gemm_clear(int* tile_count, hipStream_t stream) {
+  gemm_clear_kernel<<<1, 256, 0, stream>>>(tile_count);
+}
+
 void launch_gemm(const GemmArgs& g, int epi, hipStream_t stream) {
   if (g.M == 0) return;
-  const int m_tiles = (g.M + kBM - 1) / kBM;
-  if (epi == kSwiGLU) {
-    gemm_kernel<kSwiGLU, 128><<<dim3(unsigned(m_tiles) * unsigned(g.ffn / 64)), kGemmThreads, 0, stream>>>(g);
-    return;
-  }
-  // narrow outputs: 64-column tiles when 128-column ones would not give every CU a tile
-  const bool narrow = int64_t(m_tiles) * (g.N / 128) < 256;
-  const dim3 grid(unsigned(m_tiles) * unsigned(g.N / (narrow ? 64 : 128)));
-  if (epi == kStoreF32) {
-    if (narrow) gemm_kernel<kStoreF32, 64><<<grid, kGemmThreads, 0, stream>>>(g);
-    else gemm_kernel<kStoreF32, 128><<<grid, kGemmThreads, 0, stream>>>(g);
-  } else {
-    if (narrow) gemm_kernel<kResidual, 64><<<grid, kGemmThreads, 0, stream>>>(g);
-    else gemm_kernel<kResidual, 128><<<grid, kGemmThreads, 0, stream>>>(g);
-  }
+  if (epi == kStoreF32)
+    launch_epi<kStoreF32>(g, stream);
+  else if (epi == kResidual)
+    launch_epi<kResidual>(g, stream);
+  else
+    launch_epi<kSwiGLU>(g, stream);
 }
 
 }  // namespace epic

@@ -38,18 +38,6 @@ void launch_link_attention(const AttnArgs& a, int head_dim, int n_work, hipStrea
 // Merge split-KV partials (tiles whose key range spans several work items).
 void launch_link_combine(const AttnArgs& a, int head_dim, int n_tiles, hipStream_t stream);
 
-// Row-set GEMM C[M x N] = A[M x K] . W[N x K]^T with a fused epilogue.
-enum GemmEpilogue { kStoreF32 = 0, kResidual = 1, kSwiGLU = 2 };
-struct GemmArgs {
-  const uint16_t* A;   // [M][K] bf16
-  const uint16_t* W;   // [N][K] bf16 ([2 ffn][K] for kSwiGLU)
-  float* C;            // [M][N] fp32 output (kStoreF32) or residual (kResidual)
-  uint16_t* act;       // [M][ffn] bf16 (kSwiGLU)
-  int M, N, K, ffn;
-};
-// Requirements: K % 64 == 0; N % 128 == 0 (kStoreF32 / kResidual); ffn % 64 == 0 (kSwiGLU).
-void launch_gemm(const GemmArgs& g, int epi, hipStream_t stream);
-
 void launch_rmsnorm(const float* x, const uint16_t* w, uint16_t* out_bf16, float* out_f32, int rows, int hidden,
                     float eps, hipStream_t stream);
 void launch_rope_table(const int32_t* s_pos, float2* cs, int rows, int head_dim, double theta, hipStream_t stream);

@@ -10,9 +10,11 @@
 // and after the last layer out = RMSNorm(h) w_final.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
+#include "gemm.h"
 #include "kernels.h"
 #include "plan_internal.h"
 #include "status.h"
@@ -33,6 +35,8 @@ struct LayerWs {
   uint16_t* act;     // [n_s][ffn]
   float2* cs;        // [n_s][D/2]
   void* attn;        // split-KV partials
+  float* gemm_partial;   // GEMM tiles cut along K: partial sums
+  int* gemm_count;       // ... and their arrival counters
   size_t total;
 };
 
@@ -55,6 +59,8 @@ LayerWs carve(const epic_model_cfg* c, const epic_plan_sizes* s, char* base) {
   w.act = reinterpret_cast<uint16_t*>(take(n * size_t(c->ffn) * 2));
   w.cs = reinterpret_cast<float2*>(take(n * size_t(D / 2) * 8));
   w.attn = take(epic_link_workspace_bytes(&c->attn, s));
+  char* gw = take(gemm_workspace_bytes());
+  if (gw) gemm_workspace(gw, &w.gemm_partial, &w.gemm_count);
   w.total = off;
   return w;
 }
@@ -105,6 +111,8 @@ epic_status run_layer(const epic_model_cfg* c, const epic_layer_weights* w, cons
   g.M = n;
   g.N = (hq + 2 * hkv) * D;
   g.K = H;
+  g.partial = ws.gemm_partial;
+  g.tile_count = ws.gemm_count;
   launch_gemm(g, kStoreF32, stream);
   launch_rope_split(ws.qkv, ws.cs, ws.q, ws.k, ws.v, n, hq, hkv, D, stream);
   epic_status st = run_link_attention(&c->attn, s, p, ws.q, ws.k, ws.v, kc, vc, ws.o, nullptr, ws.attn, stream);
@@ -116,6 +124,8 @@ epic_status run_layer(const epic_model_cfg* c, const epic_layer_weights* w, cons
   g.M = n;
   g.N = H;
   g.K = hq * D;
+  g.partial = ws.gemm_partial;
+  g.tile_count = ws.gemm_count;
   launch_gemm(g, kResidual, stream);
   launch_rmsnorm(h, w->mlp_norm, ws.x, nullptr, n, H, c->rms_eps, stream);
   g = GemmArgs{};
@@ -126,6 +136,8 @@ epic_status run_layer(const epic_model_cfg* c, const epic_layer_weights* w, cons
   g.N = 2 * F;
   g.K = H;
   g.ffn = F;
+  g.partial = ws.gemm_partial;
+  g.tile_count = ws.gemm_count;
   launch_gemm(g, kSwiGLU, stream);
   g = GemmArgs{};
   g.A = ws.act;
@@ -134,6 +146,8 @@ epic_status run_layer(const epic_model_cfg* c, const epic_layer_weights* w, cons
   g.M = n;
   g.N = H;
   g.K = F;
+  g.partial = ws.gemm_partial;
+  g.tile_count = ws.gemm_count;
   launch_gemm(g, kResidual, stream);
   return hip_ok("decoder layer launch");
 }
@@ -147,6 +161,15 @@ epic_status check_common(const epic_model_cfg* c, const epic_plan_sizes* s, cons
   if (s->n_s == 0) return EPIC_OK;
   EPIC_CHECK_ARG(p->s_pos && p->tiles && p->work && p->linked_blocks, "device plan arrays are NULL");
   EPIC_CHECK_ARG(h != nullptr && (reinterpret_cast<uintptr_t>(h) & 15u) == 0, "hidden_s must be 16-byte aligned");
+  // GEMM byte offsets are 31-bit: every operand and output (rows padded to a whole
+  // 256-row tile) below 2^31 bytes
+  const int64_t rows = int64_t(s->n_s) + 256;
+  const int64_t qkv_n = int64_t(c->attn.num_q_heads + 2 * c->attn.num_kv_heads) * c->attn.head_dim;
+  const int64_t kmax = std::max<int64_t>(std::max(c->hidden, c->ffn), int64_t(c->attn.num_q_heads) * c->attn.head_dim);
+  const int64_t lim = int64_t(1) << 31;
+  if (rows * kmax * 2 >= lim || rows * std::max<int64_t>(qkv_n, c->hidden) * 4 >= lim ||
+      int64_t(4) * c->ffn * c->hidden >= lim)
+    return fail(EPIC_ERR_UNSUPPORTED, "%d rows or the weights exceed the 2^31-byte GEMM operand limit", s->n_s);
   const size_t need = carve(c, s, nullptr).total;
   if (ws == nullptr || ws_bytes < need)
     return fail(EPIC_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed", ws_bytes, need);
@@ -174,6 +197,7 @@ extern "C" epic_status epic_link_layer(const epic_model_cfg* cfg, const epic_lay
   hipStream_t s = static_cast<hipStream_t>(stream);
   const LayerWs ws = carve(cfg, sizes, static_cast<char*>(workspace));
   launch_rope_table(plan_dev->s_pos, ws.cs, sizes->n_s, cfg->attn.head_dim, cfg->rope_theta, s);
+  launch_gemm_clear(ws.gemm_count, s);
   return run_layer(cfg, w, sizes, plan_dev, hidden_s, k_cache, v_cache, ws, s);
 }
 
@@ -194,10 +218,55 @@ extern "C" epic_status epic_link_model(const epic_model_cfg* cfg, const epic_lay
   hipStream_t s = static_cast<hipStream_t>(stream);
   const LayerWs ws = carve(cfg, sizes, static_cast<char*>(workspace));
   launch_rope_table(plan_dev->s_pos, ws.cs, sizes->n_s, cfg->attn.head_dim, cfg->rope_theta, s);
+  launch_gemm_clear(ws.gemm_count, s);
   for (int l = 0; l < cfg->n_layers; ++l) {
     st = run_layer(cfg, &layers[l], sizes, plan_dev, hidden_s, k_caches[l], v_caches[l], ws, s);
     if (st != EPIC_OK) return st;
   }
   launch_rmsnorm(hidden_s, final_norm, nullptr, out_hidden, sizes->n_s, cfg->hidden, cfg->rms_eps, s);
   return hip_ok("final norm launch");
+}
+
+extern "C" size_t epic_gemm_workspace_bytes(void) { return gemm_workspace_bytes(); }
+
+extern "C" epic_status epic_gemm(int32_t epilogue, const uint16_t* a, const uint16_t* w, int32_t m, int32_t n,
+                                 int32_t k, float* c, uint16_t* act, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  clear_error();
+  EPIC_CHECK_ARG(epilogue >= EPIC_GEMM_STORE && epilogue <= EPIC_GEMM_SWIGLU, "unknown epilogue %d", epilogue);
+  EPIC_CHECK_ARG(m >= 0 && n > 0 && k > 0, "m, n, k = %d, %d, %d", m, n, k);
+  if (k % 32 != 0 || n % 128 != 0)
+    return fail(EPIC_ERR_UNSUPPORTED, "k %% 32 == 0 and n %% 128 == 0 required (k = %d, n = %d)", k, n);
+  const int64_t rows = int64_t(m) + 256, lim = int64_t(1) << 31;
+  const int64_t out_row_bytes = epilogue == EPIC_GEMM_SWIGLU ? int64_t(n / 2) * 2 : int64_t(n) * 4;
+  if (rows * k * 2 >= lim || int64_t(n) * k * 2 >= lim || rows * out_row_bytes >= lim)
+    return fail(EPIC_ERR_UNSUPPORTED, "operands of %d x %d x %d exceed the 2^31-byte limit", m, n, k);
+  if (m == 0) return EPIC_OK;
+  auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
+  EPIC_CHECK_ARG(a && w && al(a) && al(w), "a and w must be non-NULL and 16-byte aligned");
+  if (epilogue == EPIC_GEMM_SWIGLU)
+    EPIC_CHECK_ARG(act && al(act), "act must be non-NULL and 16-byte aligned");
+  else
+    EPIC_CHECK_ARG(c && al(c), "c must be non-NULL and 16-byte aligned");
+  if (workspace == nullptr || workspace_bytes < gemm_workspace_bytes())
+    return fail(EPIC_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes,
+                gemm_workspace_bytes());
+  EPIC_CHECK_ARG((reinterpret_cast<uintptr_t>(workspace) & 255u) == 0, "workspace must be 256-byte aligned");
+  GemmArgs g{};
+  g.A = a;
+  g.W = w;
+  g.M = m;
+  g.N = n;
+  g.K = k;
+  if (epilogue == EPIC_GEMM_SWIGLU) {
+    g.ffn = n / 2;
+    g.act = act;
+  } else {
+    g.C = c;
+  }
+  gemm_workspace(workspace, &g.partial, &g.tile_count);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  launch_gemm_clear(g.tile_count, s);
+  launch_gemm(g, epilogue, s);
+  return hip_ok("projection GEMM launch");
 }

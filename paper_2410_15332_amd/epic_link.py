@@ -112,9 +112,17 @@ _link_model = _proto("epic_link_model", C.c_int,
                       C.c_void_p, _P(C.c_void_p), _P(C.c_void_p), C.c_void_p, C.c_void_p, C.c_size_t,
                       C.c_void_p])
 
+_gemm_ws = _proto("epic_gemm_workspace_bytes", C.c_size_t, [])
+_gemm = _proto("epic_gemm", C.c_int,
+               [C.c_int32, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
+                C.c_void_p, C.c_size_t, C.c_void_p])
+
 EXPORTED = ["epic_status_string", "epic_last_error", "epic_version", "epic_plan_sizes_get", "epic_plan_layout",
             "epic_plan_link", "epic_link_workspace_bytes", "epic_link_attention", "epic_set_profile_events",
-            "epic_model_workspace_bytes", "epic_link_layer", "epic_link_model"]
+            "epic_model_workspace_bytes", "epic_link_layer", "epic_link_model", "epic_gemm_workspace_bytes",
+            "epic_gemm"]
+
+GEMM_STORE, GEMM_RESIDUAL, GEMM_SWIGLU = 0, 1, 2
 
 
 def _check(st: int, where: str):
@@ -279,6 +287,20 @@ def epic_link_model(cfg: epic_model_cfg, layers: Sequence[epic_layer_weights], f
     _check(_link_model(C.byref(cfg), warr, _ptr(final_norm), C.byref(dplan.sizes), C.byref(dplan.plan),
                        _ptr(hidden_s), karr, varr, _ptr(out_hidden), _ptr(workspace), ws_bytes, _stream(stream)),
            "epic_link_model")
+
+
+def epic_gemm_workspace_bytes() -> int:
+    return int(_gemm_ws())
+
+
+def epic_gemm(epilogue: int, a, w, c=None, act=None, workspace=None, stream=None):
+    """Enqueue the projection GEMM (see include/epic_link.h): a bf16 [m, k], w bf16 [n, k];
+    c fp32 [m, n] (store / residual) or act bf16 [m, n/2] (SwiGLU)."""
+    m, k = a.shape
+    n = w.shape[0]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_gemm(epilogue, _ptr(a), _ptr(w), m, n, k, _ptr(c), _ptr(act), _ptr(workspace), ws_bytes,
+                 _stream(stream)), "epic_gemm")
 
 
 # ---------------------------------------------------------------- cache layout helpers

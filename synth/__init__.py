@@ -13,4 +13,6 @@ from .gen import (  # noqa: F401
     model_weights,
     final_norm_weight,
     token_embeddings,
+    matrix_bf16,
+    matrix_f32,
 )

@@ -21,7 +21,7 @@ from typing import Dict, Sequence, Tuple
 
 import numpy as np
 
-_CHUNK, _ROW, _TOK, _W = 1, 2, 3, 4
+_CHUNK, _ROW, _TOK, _W, _MAT = 1, 2, 3, 4, 5
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -117,3 +117,16 @@ def model_weights(seed: int, layer: int, hidden: int, ffn: int, hq: int, hkv: in
 
 def final_norm_weight(seed: int, hidden: int) -> np.ndarray:
     return _norm_weight(seed, 1 << 20, W_FINAL_NORM, hidden)
+
+
+def matrix_bf16(seed: int, tag: int, shape, scale: float = 1.0) -> np.ndarray:
+    """A seeded N(0, 1) * scale matrix as bf16 bits (operands of stand-alone projection cases)."""
+    rng = np.random.default_rng([seed, _MAT, tag])
+    return _normal_bf16(rng, shape, scale)
+
+
+def matrix_f32(seed: int, tag: int, shape, scale: float = 1.0) -> np.ndarray:
+    """A seeded N(0, 1) * scale float32 matrix (e.g. a residual stream fed to a projection)."""
+    rng = np.random.default_rng([seed, _MAT, tag])
+    x = rng.standard_normal(size=shape, dtype=np.float32)
+    return x * np.float32(scale)

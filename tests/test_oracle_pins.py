@@ -344,3 +344,22 @@ def test_rope_properties():
     d1 = (oracle.rope(q, np.array([50]), 1e4) * oracle.rope(k, np.array([20]), 1e4)).sum()
     d2 = (oracle.rope(q, np.array([130]), 1e4) * oracle.rope(k, np.array([100]), 1e4)).sum()
     np.testing.assert_allclose(d1, d2, rtol=1e-12)
+
+
+def test_projection_brute_force():
+    """The projection oracle against explicit sums on tiny inputs (a dropped term,
+    a transposed operand or a swapped gate/up half changes these values)."""
+    import math
+    rng = np.random.default_rng(5)
+    m, n, k = 3, 6, 5
+    a = rng.standard_normal((m, k))
+    w = rng.standard_normal((n, k))
+    c0 = rng.standard_normal((m, n))
+    dot = [[sum(a[i, t] * w[j, t] for t in range(k)) for j in range(n)] for i in range(m)]
+    assert np.allclose(oracle.projection(a, w, "store"), dot, rtol=0, atol=1e-12)
+    assert np.allclose(oracle.projection(a, w, "residual", c0), np.asarray(dot) + c0, rtol=0, atol=1e-12)
+    f = n // 2
+    sw = [[dot[i][j] / (1.0 + math.exp(-dot[i][j])) * dot[i][j + f] for j in range(f)] for i in range(m)]
+    assert np.allclose(oracle.projection(a, w, "swiglu"), sw, rtol=0, atol=1e-12)
+    # identity weights: the store epilogue returns the rows themselves
+    assert np.array_equal(oracle.projection(a, np.eye(k), "store"), a)
