@@ -17,7 +17,7 @@ struct GemmArgs {
   uint16_t* act;       // [M][ffn] bf16 (kSwiGLU)
   int M, N, K, ffn;
   float* partial;      // split-tile partial sums, gemm_workspace_bytes() with tile_count
-  int* tile_count;     // arrival counters of split tiles; zero before the first launch
+  int* tile_count;     // arrival counters of split tiles (per wavefront); zero before the first launch
 };
 // Requirements: K % 32 == 0; N % 128 == 0 (kStoreF32 / kResidual); ffn % 128 == 0
 // (kSwiGLU); M * K and N * K below 2^30 (byte offsets of the operands fit 31 bits).

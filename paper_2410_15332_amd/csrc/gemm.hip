@@ -10,7 +10,8 @@
 // Tiling: workgroup tile 256 x TN, 8 wavefronts of 64 columns each (TN = 256:
 // 2 x 4 wavefronts of 128 x 64, i.e. 4 x 2 v_mfma_f32_32x32x16_bf16 tiles; TN = 128:
 // 4 x 2 wavefronts of 64 x 64).  K runs in stages of 32 staged in LDS by direct
-// buffer->LDS loads, NS stages in flight (loads issued NS - 1 stages ahead of use).  An operand stage is 16 groups of 16 rows; row r of a group sits at
+// buffer->LDS loads, NS stages in LDS (4 at TN = 256, 6 at TN = 128; loads issued
+// NS - 1 stages ahead of use).  An operand stage is 16 groups of 16 rows; row r of a group sits at
 // byte 64 r with its four 16-byte chunks XOR-swizzled by (r / 4) % 4, so one load
 // instruction fills one group (1 KB) and the 16 lanes of each ds_read_b128 group
 // touch distinct banks.  For kSwiGLU the TN weight rows of a tile are gate/up in
@@ -23,10 +24,10 @@
 // used and the ones that do not fill whole rounds (the last partial round plus one
 // full round, or all of them) are cut along K into G equal shares of K stages, one
 // per workgroup, so every CU gets the same work.
-// A tile cut across workgroups: each writes its fp32 partial, bumps the tile's
-// arrival counter, and the last to arrive sums the partials in K order (the result
-// does not depend on arrival order) and runs the epilogue.  No workgroup waits for
-// another.  Workgroups are dealt round-robin to the 8 XCDs; worker indices are
+// A tile cut across workgroups: each wavefront writes its fp32 partial, bumps its
+// arrival counter for the tile, and the last wavefront to arrive sums that part's
+// partials in K order (the result does not depend on arrival order) and runs its
+// epilogue.  Nothing waits for another workgroup.  Workgroups are dealt round-robin to the 8 XCDs; worker indices are
 // arranged so that each XCD works on a contiguous run of tiles, and tiles are
 // ordered in groups of up to 8 row tiles per weight tile, so concurrent workgroups
 // on an XCD share operands through its L2.
@@ -46,11 +47,12 @@ constexpr int kBufWord3 = 0x00020000;                   // gfx9 raw buffer descr
 constexpr int kMaxWorkers = 256;                        // one workgroup per CU
 constexpr int kPartialFloats = kTM * 256;               // fp32 partial sums of the largest tile
 constexpr int kMaxSplitTiles = 2 * kMaxWorkers;
+constexpr int kCounters = kMaxSplitTiles * (kThreads / 64);   // one per (cut tile, wavefront)
 constexpr int kMinUnits = 8;                            // K stages per workgroup, at least
 
 template <int TN>
 struct Shape {
-  static constexpr int NS = TN == 256 ? 4 : 6;          // LDS stages
+  static constexpr int NS = TN == 256 ? 4 : 6;          // LDS stages (128 / 144 KB)
   static constexpr int WAVES_M = TN == 256 ? 2 : 4;     // wavefronts along M
   static constexpr int WM = kTM / WAVES_M;              // rows per wavefront
   static constexpr int I = WM / 32;                     // 32-row MFMA tiles per wavefront
@@ -72,7 +74,6 @@ template <int TN>
 struct GemmLds {
   char a[Shape<TN>::NS][Shape<TN>::A_STAGE];
   char b[Shape<TN>::NS][Shape<TN>::B_STAGE];
-  int flag;
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -220,7 +221,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   // t = i*J + j, register r: row wm*WM + i*32 + (r/4)*8 + half*4 + r%4, column
   // wn*64 + j*32 + col of the workgroup tile.  Written CT tiles (CT / J row blocks)
   // at a time, so the fixup below never holds more than CT tiles of sums.
-  constexpr int CT = 2, NT = I * J, NCH = NT / CT;
+  constexpr int NT = I * J, CT = NT == 4 ? 4 : 2, NCH = NT / CT;
   const int col = lane & 31, half = lane >> 5;
   auto epilogue_part = [&](int mt, int nt, int h, const f32x16 (&v)[CT]) __attribute__((always_inline)) {
     const int m0 = mt * kTM + wm * SH::WM + half * 4;
@@ -301,11 +302,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4v, v4), rp, mine + (t * 4 + qd) * 1024, 0,
                                                kSc1);
       }
-    wait_vmem<0>();                      // this wavefront's partial has landed ...
-    barrier_lds();                       // ... and every wavefront's, before the count
-    if (tid == 0) lds.flag = atomicAdd(&g.tile_count[q], 1);
-    barrier_lds();
-    const int before = lds.flag;
+    // Each wavefront keeps its own arrival counter for the tile (its part of the
+    // tile depends only on the same wavefront's part of the other partials), so no
+    // workgroup barrier is needed: the last wavefront to arrive finishes that part.
+    wait_vmem<0>();                      // this wavefront's partial has landed
+    int* cnt = g.tile_count + q * (kThreads / 64) + wv;
+    int before = 0;
+    if (lane == 0) before = atomicAdd(cnt, 1);
+    before = __builtin_amdgcn_readfirstlane(before);
     if (before != wl - wf) return;       // not the last to arrive
 #pragma unroll
     for (int h = 0; h < NCH; ++h) {      // sum the partials in K order, CT tiles at a time
@@ -326,7 +330,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
       }
       epilogue_part(mt, nt, h, v);
     }
-    if (tid == 0) atomicExch(&g.tile_count[q], 0);   // ready for the next launch
+    if (lane == 0) atomicExch(cnt, 0);   // ready for the next launch
   };
 
   // ---- pipeline: unit u (one K stage of one tile) lives in LDS buffer u % NS.
@@ -334,7 +338,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   // waits for this wavefront's loads of unit u + 1, and after the barrier (all
   // loads of u + 1 visible, every read of buffer u % NS done) refills that buffer
   // with unit u + NS and reads the first k-slice of u + 1.  Loads past the last
-  // unit repeat it, so every step leaves the same number in flight.
+  // unit repeat it, so every step leaves the same number in flight.  (One barrier
+  // per two units measured slower at TN = 128.)
   Cursor cc, dc;
   seek(cc, 0);
   dc = cc;
@@ -380,7 +385,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
 }
 
 __global__ void gemm_clear_kernel(int* cnt) {
-  for (int i = threadIdx.x; i < kMaxSplitTiles; i += blockDim.x) cnt[i] = 0;
+  for (int i = threadIdx.x; i < kCounters; i += blockDim.x) cnt[i] = 0;
 }
 
 int cdiv(int a, int b) { return (a + b - 1) / b; }
@@ -425,7 +430,7 @@ void launch_epi(const GemmArgs& g, hipStream_t stream) {
 }  // namespace
 
 size_t gemm_workspace_bytes() {
-  return size_t(2 * kMaxWorkers) * kPartialFloats * sizeof(float) + kMaxSplitTiles * sizeof(int);
+  return size_t(2 * kMaxWorkers) * kPartialFloats * sizeof(float) + kCounters * sizeof(int);
 }
 
 void gemm_workspace(void* base, float** partial, int** tile_count) {
