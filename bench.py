@@ -41,6 +41,9 @@ WORKLOADS = {
     "c2": ("c2", {}),
     "c1": ("c1", {}),
     "c3": ("c3", {}),
+    # decode after the link step (one new token per request), not the default line
+    "c5k32dec": ("c5", {"k": 32}),
+    "c4dec": ("c4", {}),
 }
 
 
@@ -209,6 +212,59 @@ def bench_model(args, wl):
     print(json.dumps(result), flush=True)
 
 
+def bench_decode(args, wl):
+    """Decode after the link step: one new token per request attends over its linked
+    sequence (link step run once, untimed; the same decode step is then timed).  The
+    attention kernel reads each request's K/V once: roofline against HBM, algorithmic
+    bytes = sum over requests of (linked tokens + 1) x Hkv x D x 2 B x 2 (K and V)."""
+    import numpy as np
+    import torch
+
+    from paper_2410_15332_amd import epic_link as el
+    from paper_2410_15332_amd import harness
+
+    st = harness.stage_attention(wl, device="cuda", spare_blocks=4 * wl.batch)
+    st.run()
+    ds = harness.stage_decode(wl, st.cfg, st.sizes, st.dplan.host, st.spare, st.num_blocks, [1] * wl.batch)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        ds.run(st.k_cache, st.v_cache)
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for e in (x for row in ev for x in row):
+        e.record()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(K):
+        el.epic_set_profile_events(ev[i])
+        ds.run(st.k_cache, st.v_cache)
+    end.record()
+    el.epic_set_profile_events(None)
+    torch.cuda.synchronize()
+    step_ms = start.elapsed_time(end) / K
+    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    comb_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
+    linked = ds.views["s_pos"].astype(np.int64) + 1
+    kv_bytes = float(linked.sum()) * wl.num_kv_heads * wl.head_dim * 2 * 2
+    gbs = kv_bytes / (attn_ms * 1e-3) / 1e9
+    log(f"decode step {step_ms:.4f} ms: attention {attn_ms:.4f} ms ({gbs:.0f} GB/s of K/V), combine {comb_ms:.4f}")
+    result = {
+        "metric": "decode step (ms) + tokens/s; attention K/V GB/s vs HBM peak", "value": round(wl.batch / (step_ms * 1e-3), 1),
+        "unit": "decoded tokens/s", "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": round(step_ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 chunk caches and q/k/v)",
+        "config": {"workload": wl.name + "_decode1", "batch": wl.batch, "k": wl.k, "num_q_heads": wl.num_q_heads,
+                   "num_kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim,
+                   "linked_tokens_per_request": int(linked.max()), "parallelism": "single GPU"},
+        "kernel_ms": {"attention": round(attn_ms, 5), "combine": round(comb_ms, 5)},
+        "roofline": {"bound": "hbm", "kernel": f"link_attention_kernel<{wl.head_dim}, {ds.sizes.tile_rows // 32}>",
+                     "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "algorithmic_bytes_per_launch": kv_bytes, "traffic": None},
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -239,6 +295,9 @@ def main():
     wl = get_config(name, **kw)
     if name == "c3":
         bench_model(args, wl)
+        return
+    if args.workload.endswith("dec"):
+        bench_decode(args, wl)
         return
     t0 = time.time()
     st = harness.stage_attention(wl, device="cuda", split_blocks=args.split_blocks)

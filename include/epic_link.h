@@ -159,6 +159,25 @@ epic_status epic_plan_link(const epic_link_request* reqs, int32_t batch,
                            int32_t n_free, int32_t num_blocks,
                            const epic_plan_sizes* sizes, epic_plan* plan);
 
+/* Decode over the linked cache (the step after the link: each request appends
+ * new tokens after its last linked position and only those are computed).
+ * prev / prev_sizes: the host arrays of the previous plan of these requests (the
+ * link plan, or the previous decode plan).  new_tokens[b] >= 0 tokens are
+ * appended to request b: S = those, at positions n_b .. n_b + t_b - 1 where n_b is
+ * the request's linked length in prev.  They fill the request's last block if the
+ * previous plan wrote it (a private block) and it has free slots -- that block is
+ * its own copy source, so its earlier tokens stay -- and then new blocks taken in
+ * order from free_blocks (distinct, not linked by prev).  The new plan links
+ * everything prev linked plus the new blocks; it lists as private only the blocks
+ * that receive a new token, so epic_link_attention with it (q_s / k_s / v_s of the
+ * new tokens) writes nothing else.  Host only, integer, synchronous. */
+epic_status epic_plan_decode_sizes(const epic_plan_sizes* prev_sizes, const epic_plan* prev,
+                                   const int32_t* new_tokens, const epic_attn_cfg* cfg, int32_t n_free,
+                                   epic_plan_sizes* out);
+epic_status epic_plan_decode(const epic_plan_sizes* prev_sizes, const epic_plan* prev, const int32_t* new_tokens,
+                             const epic_attn_cfg* cfg, const int32_t* free_blocks, int32_t n_free,
+                             int32_t num_blocks, const epic_plan_sizes* sizes, epic_plan* plan);
+
 /* Workspace bytes epic_link_attention needs for this plan (split-KV partials). */
 size_t epic_link_workspace_bytes(const epic_attn_cfg* cfg, const epic_plan_sizes* sizes);
 

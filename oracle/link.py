@@ -129,3 +129,26 @@ def link_attention(chunk_lens: Sequence[int], suffix_len: int, k: int,
     K_exp, V_exp = expand_kv(cached_k, cached_v, s_pos, k_s, v_s, n_total)
     out, lse = masked_attention(q_s, K_exp, V_exp, s_pos, scale, rows)
     return s_pos, out, lse, K_exp, V_exp
+
+
+def decode_attention(chunk_lens: Sequence[int], suffix_len: int, k: int,
+                     cached_k: Sequence[np.ndarray], cached_v: Sequence[np.ndarray],
+                     k_s: np.ndarray, v_s: np.ndarray,
+                     new_q: np.ndarray, new_k: np.ndarray, new_v: np.ndarray,
+                     scale: float | None = None):
+    """Decode after the link step, for one request: t new tokens appended after the
+    N = sum(chunk_lens) + suffix_len linked tokens attend, causally, over the linked
+    sequence (K_exp / V_exp of the link step, Sec. 4.2) extended by themselves.
+
+    k_s, v_s: the link step's recomputed rows of S (ascending); new_q / new_k /
+    new_v: [t, H, d] rows of the new tokens at positions N .. N + t - 1.
+    Returns (new_pos, out, lse, K_exp, V_exp) with K_exp / V_exp [N + t, Hkv, d].
+    """
+    s_pos = legolink_positions(chunk_lens, suffix_len, k)
+    n_total = sum(int(x) for x in chunk_lens) + suffix_len
+    t = new_q.shape[0]
+    new_pos = np.arange(n_total, n_total + t, dtype=np.int64)
+    K_exp, V_exp = expand_kv(cached_k, cached_v, np.concatenate([s_pos, new_pos]),
+                             np.concatenate([k_s, new_k]), np.concatenate([v_s, new_v]), n_total + t)
+    out, lse = masked_attention(new_q, K_exp, V_exp, new_pos, scale)
+    return new_pos, out, lse, K_exp, V_exp

@@ -534,13 +534,18 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
 }
 
 // Merge the split-KV partials of a tile: lse = log2 sum_i 2^lse_i, out = sum_i 2^(lse_i - lse) O_i.
-// Workgroup = (tile, KV head, quarter of the head dim); thread = (tile row, half of that quarter).
+// Workgroup = (tile, KV head, quarter of the head dim).  Each (valid tile row, half
+// of that quarter) gets P lanes of one wavefront (P a power of two, at most 64, the
+// number of partials, and 512 / (2 x valid rows)); lane j takes partials j, j + P, ..., and the lanes
+// combine their (max, weight sum, weighted sums) by butterfly exchanges.  A tile
+// of few rows (decode: one row per head) with many partials so gets the whole
+// workgroup's memory parallelism.
 constexpr int kCombineParts = 4;
-constexpr int kCombineThreads = 512;   // 2 x the largest tile
+constexpr int kCombineThreads = 512;
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void link_combine_kernel(AttnArgs a) {
   constexpr int DQ = D / kCombineParts;       // dims per workgroup
-  constexpr int DT = DQ / 2;                  // dims per thread (16 or 8)
+  constexpr int DT = DQ / 2;                  // dims per (row, half)
   const int hkv = a.hkv;
   const int dq = blockIdx.x % kCombineParts;
   const int g = (blockIdx.x / kCombineParts) % hkv;
@@ -548,24 +553,30 @@ __global__ __launch_bounds__(kCombineThreads) void link_combine_kernel(AttnArgs 
   const int p0 = a.tiles[4 * tile + 2];
   const int ns = a.tiles[4 * tile + 3];
   if (p0 < 0) return;
-  const int row0 = a.tiles[4 * tile + 0], nrows = a.tiles[4 * tile + 1];
-  const int t = threadIdx.x >> 1, hf = threadIdx.x & 1;
-  const int TR = a.tile_rows;
-  if (t >= TR) return;
-  const int R = a.rows_per_tile;
-  const int srl = t % R, h = g * a.G + t / R;
-  if (srl >= nrows) return;
-  const int srow = row0 + srl;
+  const int nrows = a.tiles[4 * tile + 1];
+  const int R = a.rows_per_tile, TR = a.tile_rows;
+  const int n_valid = nrows * a.G;            // tile rows t = head * R + s, s < nrows
+  const int pairs = 2 * n_valid;
+  int P = 64;                                 // lanes per (row, half): no more than partials
+  while (P > 1 && (P * pairs > kCombineThreads || P > ns)) P >>= 1;
+  const int pair = threadIdx.x / P, j = threadIdx.x % P;
+  if (pair >= pairs) return;                  // whole groups of P lanes leave together
+  const int vr = pair >> 1, hf = pair & 1;
+  const int hh = vr / nrows, srl = vr % nrows;
+  const int t = hh * R + srl;
+  const int srow = a.tiles[4 * tile + 0] + srl;
+  const int h = g * a.G + hh;
   const int d0 = dq * DQ + hf * DT;
+  auto lse_of = [&](int i) { return a.part_lse[(size_t(p0 + i) * hkv + g) * TR + t]; };
   float mx = -INFINITY;
-  for (int i = 0; i < ns; ++i) mx = fmaxf(mx, a.part_lse[(size_t(p0 + i) * hkv + g) * TR + t]);
+  for (int i = j; i < ns; i += P) mx = fmaxf(mx, lse_of(i));
+  for (int o = 1; o < P; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
   float acc[DT];
 #pragma unroll
   for (int d = 0; d < DT; ++d) acc[d] = 0.0f;
   float wsum = 0.0f;
-  for (int i = 0; i < ns; ++i) {
-    const float l = a.part_lse[(size_t(p0 + i) * hkv + g) * TR + t];
-    const float w = fast_exp2(l - mx);
+  for (int i = j; i < ns; i += P) {
+    const float w = fast_exp2(lse_of(i) - mx);
     wsum += w;
     const float* pp = a.part_o + ((size_t(p0 + i) * hkv + g) * TR + t) * D + d0;
 #pragma unroll
@@ -577,6 +588,12 @@ __global__ __launch_bounds__(kCombineThreads) void link_combine_kernel(AttnArgs 
       acc[d + 3] += w * f.w;
     }
   }
+  for (int o = 1; o < P; o <<= 1) {
+    wsum += __shfl_xor(wsum, o);
+#pragma unroll
+    for (int d = 0; d < DT; ++d) acc[d] += __shfl_xor(acc[d], o);
+  }
+  if (j != 0) return;
   const float inv = 1.0f / wsum;
   uint16_t* op = a.out + (size_t(srow) * a.hq + h) * D + d0;
 #pragma unroll

@@ -113,22 +113,23 @@ struct Tile {
   int req, row0, nrows, nblk;
 };
 
+// S positions and linked-block first positions of one request.
+struct ReqRows {
+  std::vector<int32_t> pos, p0;
+};
+
 // Query tiles: consecutive S rows of one request, rows_per_tile at a time.  A
 // tile needs the linked blocks whose first position is <= its last row's position.
-void make_tiles(const epic_link_request* reqs, int batch, int rows_per_tile, std::vector<Tile>* tiles,
-                int64_t* total_blocks) {
-  *total_blocks = 0;
+void make_tiles(const std::vector<ReqRows>& rr, int rows_per_tile, std::vector<Tile>* tiles) {
   int row_base = 0;
-  for (int b = 0; b < batch; ++b) {
-    std::vector<int32_t> pos, p0, ln;
-    select_positions(reqs[b], &pos);
-    linked_blocks(reqs[b], &p0, &ln);
+  for (size_t b = 0; b < rr.size(); ++b) {
+    const std::vector<int32_t>& pos = rr[b].pos;
+    const std::vector<int32_t>& p0 = rr[b].p0;
     for (size_t r0 = 0; r0 < pos.size(); r0 += rows_per_tile) {
       const int n = static_cast<int>(std::min<size_t>(rows_per_tile, pos.size() - r0));
       const int32_t last = pos[r0 + n - 1];
       const int nblk = static_cast<int>(std::upper_bound(p0.begin(), p0.end(), last) - p0.begin());
-      tiles->push_back(Tile{b, row_base + static_cast<int>(r0), n, nblk});
-      *total_blocks += nblk;
+      tiles->push_back(Tile{static_cast<int>(b), row_base + static_cast<int>(r0), n, nblk});
     }
     row_base += static_cast<int>(pos.size());
   }
@@ -238,7 +239,106 @@ using namespace epic;
 
 namespace {
 
-// Sizes of the plan, plus its attention tiles and split (shared by the sizes
+// Tile size and split-KV split for these S rows; fills s->tile_rows, n_tiles,
+// n_work, n_partials.  256-row tiles share each staged K/V block between twice
+// the rows, which pays when their rows need the same keys: take them when they
+// cost at most 1% more (row x 64-key) steps than 128-row tiles -- rows of one
+// stretch of positions (recompute-all, suffix-only) rather than the first k rows
+// of several chunks -- and still give every CU a workgroup.
+void choose_tiles(const std::vector<ReqRows>& rr, const epic_attn_cfg* cfg, epic_plan_sizes* s,
+                  std::vector<Tile>* tiles_out, int* split_out) {
+  const int G = cfg->num_q_heads / cfg->num_kv_heads;
+  std::vector<Tile>& tiles = *tiles_out;
+  std::vector<Tile> small, large;
+  make_tiles(rr, kTileRowsSmall / G, &small);
+  make_tiles(rr, kTileRowsLarge / G, &large);
+  auto row_steps = [](const std::vector<Tile>& ts, int rows) {
+    int64_t n = 0;
+    for (const Tile& t : ts) n += int64_t(cdiv(t.nblk, kKvTileBlocks)) * rows;
+    return n;
+  };
+  double est = 0.0;
+  int split = split_blocks(cfg, large, kShapeLarge, &est);
+  int64_t large_items = 0;
+  for (const Tile& t : large) large_items += std::max(1, cdiv(t.nblk, split));
+  const bool use_large = cfg->tile_rows != 0
+                             ? cfg->tile_rows == kTileRowsLarge
+                             : row_steps(large, kTileRowsLarge) * 100 <= row_steps(small, kTileRowsSmall) * 101 &&
+                                   large_items * cfg->num_kv_heads >= kShapeLarge.slots;
+  if (use_large) {
+    tiles.swap(large);
+    s->tile_rows = kTileRowsLarge;
+  } else {
+    tiles.swap(small);
+    s->tile_rows = kTileRowsSmall;
+    split = split_blocks(cfg, tiles, kShapeSmall, &est);
+  }
+  *split_out = split;
+  int64_t n_work = 0, n_part = 0;
+  for (const Tile& t : tiles) {
+    const int ns = std::max(1, cdiv(t.nblk, split));
+    n_work += ns;
+    if (ns > 1) n_part += ns;
+  }
+  s->n_tiles = static_cast<int32_t>(tiles.size());
+  s->n_work = static_cast<int32_t>(n_work);
+  s->n_partials = static_cast<int32_t>(n_part);
+}
+
+void finish_sizes(epic_plan_sizes* s) {
+  s->total_ints = 3 * align16(s->n_s) + 2 * align16(s->batch + 1) + 3 * align16(s->n_linked_blocks) +
+                  2 * align16(s->n_private) + align16(int64_t(s->n_private) * kBlock) +
+                  align16(4 * int64_t(s->n_tiles)) + align16(kWorkInts * int64_t(s->n_work));
+}
+
+// Attention tiles and split-KV work items of a plan whose S rows and linked
+// tables are written.  Work items are ordered key segment first, so that the
+// workgroups running at the same time read the same KV blocks (one L2 per XCD
+// serves them).
+epic_status write_work(const std::vector<Tile>& tiles, int split, const epic_plan_sizes& chk, epic_plan* plan) {
+  int part = 0;
+  for (size_t t = 0; t < tiles.size(); ++t) {
+    const int ns = std::max(1, cdiv(tiles[t].nblk, split));
+    plan->tiles[4 * t + 0] = tiles[t].row0;
+    plan->tiles[4 * t + 1] = tiles[t].nrows;
+    plan->tiles[4 * t + 2] = ns > 1 ? part : -1;
+    plan->tiles[4 * t + 3] = ns;
+    if (ns > 1) part += ns;
+  }
+  // work items in launch order (segment-major, longest key range first)
+  int w = 0;
+  for (const auto& [t, seg] : item_order(tiles, split)) {
+    const int ns = plan->tiles[4 * t + 3];
+    const int base = plan->blk_off[tiles[t].req];
+    const int b0 = base + seg * split;
+    const int b1 = base + std::min(tiles[t].nblk, (seg + 1) * split);
+    // Leading KV tiles (kKvTileBlocks blocks each) that need no mask: all
+    // blocks full and every key at or before the tile's first row.
+    const int32_t first_pos = plan->s_pos[tiles[t].row0];
+    int n_fast = 0;
+    for (int b = b0; b + kKvTileBlocks <= b1; b += kKvTileBlocks) {
+      bool ok = true;
+      for (int i = 0; i < kKvTileBlocks; ++i) ok = ok && plan->block_len[b + i] == kBlock;
+      const int last = b + kKvTileBlocks - 1;
+      ok = ok && plan->block_pos0[last] + kBlock - 1 <= first_pos;
+      if (!ok) break;
+      ++n_fast;
+    }
+    int32_t* wk = plan->work + int64_t(kWorkInts) * w;
+    wk[0] = static_cast<int32_t>(t);
+    wk[1] = b0;
+    wk[2] = b1;
+    wk[3] = ns > 1 ? plan->tiles[4 * t + 2] + seg : -1;
+    wk[4] = n_fast;
+    wk[5] = wk[6] = wk[7] = 0;
+    ++w;
+  }
+  if (w != chk.n_work || part != chk.n_partials)
+    return fail(EPIC_ERR_INVALID_ARG, "internal planner inconsistency (work)");
+  return EPIC_OK;
+}
+
+// Sizes of the link plan, plus its attention tiles and split (shared by the sizes
 // query and the plan builder, so the split search runs once per call).
 epic_status plan_shape(const epic_link_request* reqs, int32_t batch, const epic_attn_cfg* cfg, int32_t n_free,
                        epic_plan_sizes* out, std::vector<Tile>* tiles_out, int* split_out) {
@@ -263,54 +363,18 @@ epic_status plan_shape(const epic_link_request* reqs, int32_t batch, const epic_
   EPIC_CHECK_ARG(n_s < (int64_t(1) << 30) && n_lb < (int64_t(1) << 30), "batch too large");
   if (n_priv > n_free)
     return fail(EPIC_ERR_NO_PRIVATE_BLOCKS, "plan needs %lld private blocks, %d free", (long long)n_priv, n_free);
-  // Tile size.  256-row tiles share each staged K/V block between twice the
-  // rows, which pays when their rows need the same keys: take them when they
-  // cost at most 1% more (row x 64-key) steps than 128-row tiles -- rows of
-  // one stretch of positions (recompute-all, suffix-only) rather than the
-  // first k rows of several chunks -- and still give every CU a workgroup.
-  const int G = cfg->num_q_heads / cfg->num_kv_heads;
-  std::vector<Tile>& tiles = *tiles_out;
-  std::vector<Tile> small, large;
-  int64_t total_blocks = 0;
-  make_tiles(reqs, batch, kTileRowsSmall / G, &small, &total_blocks);
-  make_tiles(reqs, batch, kTileRowsLarge / G, &large, &total_blocks);
-  auto row_steps = [](const std::vector<Tile>& ts, int rows) {
-    int64_t n = 0;
-    for (const Tile& t : ts) n += int64_t(cdiv(t.nblk, kKvTileBlocks)) * rows;
-    return n;
-  };
-  double est = 0.0;
-  int split = split_blocks(cfg, large, kShapeLarge, &est);
-  int64_t large_items = 0;
-  for (const Tile& t : large) large_items += std::max(1, cdiv(t.nblk, split));
-  const bool use_large = cfg->tile_rows != 0
-                             ? cfg->tile_rows == kTileRowsLarge
-                             : row_steps(large, kTileRowsLarge) * 100 <= row_steps(small, kTileRowsSmall) * 101 &&
-                                   large_items * cfg->num_kv_heads >= kShapeLarge.slots;
-  if (use_large) {
-    tiles.swap(large);
-    s.tile_rows = kTileRowsLarge;
-  } else {
-    tiles.swap(small);
-    s.tile_rows = kTileRowsSmall;
-    split = split_blocks(cfg, tiles, kShapeSmall, &est);
+  std::vector<ReqRows> rr(static_cast<size_t>(batch));
+  for (int b = 0; b < batch; ++b) {
+    std::vector<int32_t> ln;
+    select_positions(reqs[b], &rr[b].pos);
+    linked_blocks(reqs[b], &rr[b].p0, &ln);
   }
-  *split_out = split;
-  int64_t n_work = 0, n_part = 0;
-  for (const Tile& t : tiles) {
-    const int ns = std::max(1, cdiv(t.nblk, split));
-    n_work += ns;
-    if (ns > 1) n_part += ns;
-  }
+  choose_tiles(rr, cfg, &s, tiles_out, split_out);
   s.n_s = static_cast<int32_t>(n_s);
   s.n_linked_blocks = static_cast<int32_t>(n_lb);
   s.n_private = static_cast<int32_t>(n_priv);
-  s.n_tiles = static_cast<int32_t>(tiles.size());
-  s.n_work = static_cast<int32_t>(n_work);
-  s.n_partials = static_cast<int32_t>(n_part);
   s.max_pos = static_cast<int32_t>(max_pos);
-  s.total_ints = 3 * align16(n_s) + 2 * align16(batch + 1) + 3 * align16(n_lb) + 2 * align16(n_priv) +
-                 align16(n_priv * kBlock) + align16(4 * int64_t(tiles.size())) + align16(kWorkInts * n_work);
+  finish_sizes(&s);
   *out = s;
   return EPIC_OK;
 }
@@ -455,49 +519,164 @@ extern "C" epic_status epic_plan_link(const epic_link_request* reqs, int32_t bat
   if (row != chk.n_s || lb != chk.n_linked_blocks || pv != chk.n_private)
     return fail(EPIC_ERR_INVALID_ARG, "internal planner inconsistency");
 
-  // Attention tiles and split-KV work items.  Work items are ordered key
-  // segment first, so that the workgroups running at the same time read the
-  // same KV blocks (one L2 per XCD serves them).
-  int part = 0;
-  for (size_t t = 0; t < tiles.size(); ++t) {
-    const int ns = std::max(1, cdiv(tiles[t].nblk, split));
-    plan->tiles[4 * t + 0] = tiles[t].row0;
-    plan->tiles[4 * t + 1] = tiles[t].nrows;
-    plan->tiles[4 * t + 2] = ns > 1 ? part : -1;
-    plan->tiles[4 * t + 3] = ns;
-    if (ns > 1) part += ns;
+  return write_work(tiles, split, chk, plan);
+}
+
+// ---------------------------------------------------------------- decode
+
+namespace {
+
+// One request of a decode plan: its blocks in the previous plan, its length there,
+// the free slots of its last block when that block may take the new tokens, and
+// the new blocks it needs.
+struct DecodeReq {
+  int a = 0, e = 0;        // linked blocks [a, e) of the previous plan
+  int64_t n = 0;           // tokens linked so far
+  int t = 0;               // new tokens
+  int room = 0;            // new tokens that go into the last block
+  int extra = 0;           // new blocks
+};
+
+epic_status decode_shape(const epic_plan_sizes* ps, const epic_plan* prev, const int32_t* new_tokens,
+                         const epic_attn_cfg* cfg, int32_t n_free, epic_plan_sizes* out,
+                         std::vector<Tile>* tiles_out, int* split_out, std::vector<DecodeReq>* dr_out) {
+  EPIC_CHECK_ARG(ps && prev && out, "NULL previous plan, sizes or output");
+  EPIC_CHECK_ARG(n_free >= 0, "n_free %d < 0", n_free);
+  epic_status st = validate_attn_cfg(cfg);
+  if (st != EPIC_OK) return st;
+  const int batch = ps->batch;
+  EPIC_CHECK_ARG(batch == 0 || (new_tokens && prev->blk_off && prev->linked_blocks && prev->block_pos0 &&
+                                prev->block_len),
+                 "NULL new_tokens or previous plan array");
+  EPIC_CHECK_ARG(ps->n_private == 0 || prev->priv_block, "previous plan has no private block list");
+  // blocks the previous step wrote: only those may take further tokens
+  std::vector<int32_t> written(prev->priv_block, prev->priv_block + ps->n_private);
+  std::sort(written.begin(), written.end());
+  std::vector<DecodeReq>& dr = *dr_out;
+  dr.assign(static_cast<size_t>(batch), DecodeReq{});
+  std::vector<ReqRows> rr(static_cast<size_t>(batch));
+  int64_t n_s = 0, n_lb = 0, n_priv = 0, n_take = 0, max_pos = 0;
+  for (int b = 0; b < batch; ++b) {
+    DecodeReq& d = dr[b];
+    d.a = prev->blk_off[b];
+    d.e = prev->blk_off[b + 1];
+    EPIC_CHECK_ARG(0 <= d.a && d.a <= d.e && d.e <= ps->n_linked_blocks, "previous plan: bad blk_off at %d", b);
+    d.t = new_tokens[b];
+    EPIC_CHECK_ARG(d.t >= 0, "request %d: %d new tokens", b, d.t);
+    for (int i = d.a; i < d.e; ++i) rr[b].p0.push_back(prev->block_pos0[i]);
+    if (d.e > d.a) {
+      const int last = d.e - 1, len = prev->block_len[last];
+      d.n = int64_t(prev->block_pos0[last]) + len;
+      if (len < kBlock && std::binary_search(written.begin(), written.end(), prev->linked_blocks[last]))
+        d.room = std::min(d.t, kBlock - len);
+    }
+    d.extra = cdiv(d.t - d.room, kBlock);
+    EPIC_CHECK_ARG(d.n + d.t < (int64_t(1) << 30), "request %d: too many tokens", b);
+    for (int i = 0; i < d.extra; ++i) rr[b].p0.push_back(static_cast<int32_t>(d.n + d.room + int64_t(i) * kBlock));
+    for (int i = 0; i < d.t; ++i) rr[b].pos.push_back(static_cast<int32_t>(d.n + i));
+    n_s += d.t;
+    n_lb += (d.e - d.a) + d.extra;
+    n_priv += (d.room > 0 ? 1 : 0) + d.extra;
+    n_take += d.extra;
+    max_pos = std::max<int64_t>(max_pos, d.n + d.t);
   }
-  // work items in launch order (segment-major, longest key range first)
-  int w = 0;
-  for (const auto& [t, seg] : item_order(tiles, split)) {
-    {
-      const int ns = plan->tiles[4 * t + 3];
-      const int base = plan->blk_off[tiles[t].req];
-      const int b0 = base + seg * split;
-      const int b1 = base + std::min(tiles[t].nblk, (seg + 1) * split);
-      // Leading KV tiles (kKvTileBlocks blocks each) that need no mask: all
-      // blocks full and every key at or before the tile's first row.
-      const int32_t first_pos = plan->s_pos[tiles[t].row0];
-      int n_fast = 0;
-      for (int b = b0; b + kKvTileBlocks <= b1; b += kKvTileBlocks) {
-        bool ok = true;
-        for (int i = 0; i < kKvTileBlocks; ++i) ok = ok && plan->block_len[b + i] == kBlock;
-        const int last = b + kKvTileBlocks - 1;
-        ok = ok && plan->block_pos0[last] + kBlock - 1 <= first_pos;
-        if (!ok) break;
-        ++n_fast;
-      }
-      int32_t* wk = plan->work + int64_t(kWorkInts) * w;
-      wk[0] = static_cast<int32_t>(t);
-      wk[1] = b0;
-      wk[2] = b1;
-      wk[3] = ns > 1 ? plan->tiles[4 * t + 2] + seg : -1;
-      wk[4] = n_fast;
-      wk[5] = wk[6] = wk[7] = 0;
-      ++w;
+  EPIC_CHECK_ARG(n_s < (int64_t(1) << 30) && n_lb < (int64_t(1) << 30), "batch too large");
+  if (n_take > n_free)
+    return fail(EPIC_ERR_NO_PRIVATE_BLOCKS, "plan needs %lld new blocks, %d free", (long long)n_take, n_free);
+  epic_plan_sizes s{};
+  s.batch = batch;
+  choose_tiles(rr, cfg, &s, tiles_out, split_out);
+  s.n_s = static_cast<int32_t>(n_s);
+  s.n_linked_blocks = static_cast<int32_t>(n_lb);
+  s.n_private = static_cast<int32_t>(n_priv);
+  s.max_pos = static_cast<int32_t>(max_pos);
+  finish_sizes(&s);
+  *out = s;
+  return EPIC_OK;
+}
+
+}  // namespace
+
+extern "C" epic_status epic_plan_decode_sizes(const epic_plan_sizes* prev_sizes, const epic_plan* prev,
+                                              const int32_t* new_tokens, const epic_attn_cfg* cfg, int32_t n_free,
+                                              epic_plan_sizes* out) {
+  clear_error();
+  std::vector<Tile> tiles;
+  std::vector<DecodeReq> dr;
+  int split = 0;
+  return decode_shape(prev_sizes, prev, new_tokens, cfg, n_free, out, &tiles, &split, &dr);
+}
+
+extern "C" epic_status epic_plan_decode(const epic_plan_sizes* prev_sizes, const epic_plan* prev,
+                                        const int32_t* new_tokens, const epic_attn_cfg* cfg,
+                                        const int32_t* free_blocks, int32_t n_free, int32_t num_blocks,
+                                        const epic_plan_sizes* sizes, epic_plan* plan) {
+  clear_error();
+  epic_plan_sizes chk;
+  std::vector<Tile> tiles;
+  std::vector<DecodeReq> dr;
+  int split = 0;
+  epic_status st = decode_shape(prev_sizes, prev, new_tokens, cfg, n_free, &chk, &tiles, &split, &dr);
+  if (st != EPIC_OK) return st;
+  EPIC_CHECK_ARG(sizes && plan, "NULL sizes or plan");
+  EPIC_CHECK_ARG(std::memcmp(&chk, sizes, sizeof(chk)) == 0, "sizes do not match this previous plan");
+  EPIC_CHECK_ARG(num_blocks > 0, "num_blocks %d <= 0", num_blocks);
+  int64_t n_take = 0;
+  for (const DecodeReq& d : dr) n_take += d.extra;
+  EPIC_CHECK_ARG(n_take == 0 || free_blocks != nullptr, "free_blocks is NULL");
+  // free blocks: in range, distinct, not linked by the previous plan
+  std::vector<uint8_t> used(static_cast<size_t>(num_blocks), 0);
+  for (int i = 0; i < prev_sizes->n_linked_blocks; ++i) {
+    const int id = prev->linked_blocks[i];
+    EPIC_CHECK_ARG(id >= 0 && id < num_blocks, "previous plan: block id %d out of range [0, %d)", id, num_blocks);
+    used[id] = 1;
+  }
+  for (int64_t i = 0; i < n_take; ++i) {
+    const int id = free_blocks[i];
+    EPIC_CHECK_ARG(id >= 0 && id < num_blocks, "free block id %d out of range [0, %d)", id, num_blocks);
+    EPIC_CHECK_ARG(used[id] == 0, "free block %d is already linked or listed twice", id);
+    used[id] = 2;
+  }
+  const int bs = kBlock;
+  int row = 0, lb = 0, pv = 0, fl = 0;
+  auto add_row = [&](int b, int64_t pos, int id, int o) {
+    plan->s_pos[row] = static_cast<int32_t>(pos);
+    plan->s_req[row] = b;
+    plan->s_slot[row] = id * bs + o;
+    return row++;
+  };
+  for (int b = 0; b < chk.batch; ++b) {
+    const DecodeReq& d = dr[b];
+    plan->s_off[b] = row;
+    plan->blk_off[b] = lb;
+    for (int i = d.a; i < d.e; ++i, ++lb) {
+      plan->linked_blocks[lb] = prev->linked_blocks[i];
+      plan->block_pos0[lb] = prev->block_pos0[i];
+      plan->block_len[lb] = prev->block_len[i] + (i == d.e - 1 ? d.room : 0);
+    }
+    int64_t pos = d.n;
+    if (d.room > 0) {                          // the last block takes the first new tokens
+      const int id = prev->linked_blocks[d.e - 1], len = prev->block_len[d.e - 1];
+      plan->priv_block[pv] = id;
+      plan->priv_src[pv] = id;                 // its earlier tokens stay: copied onto themselves
+      for (int o = 0; o < bs; ++o)
+        plan->priv_rows[int64_t(pv) * bs + o] = (o >= len && o < len + d.room) ? add_row(b, pos++, id, o) : -1;
+      ++pv;
+    }
+    for (int i = 0; i < d.extra; ++i, ++lb, ++pv) {
+      const int id = free_blocks[fl++];
+      const int len = static_cast<int>(std::min<int64_t>(bs, d.n + d.t - pos));
+      plan->linked_blocks[lb] = id;
+      plan->block_pos0[lb] = static_cast<int32_t>(pos);
+      plan->block_len[lb] = len;
+      plan->priv_block[pv] = id;
+      plan->priv_src[pv] = -1;
+      for (int o = 0; o < bs; ++o) plan->priv_rows[int64_t(pv) * bs + o] = o < len ? add_row(b, pos++, id, o) : -1;
     }
   }
-  if (w != chk.n_work || part != chk.n_partials)
-    return fail(EPIC_ERR_INVALID_ARG, "internal planner inconsistency (work)");
-  return EPIC_OK;
+  plan->s_off[chk.batch] = row;
+  plan->blk_off[chk.batch] = lb;
+  if (row != chk.n_s || lb != chk.n_linked_blocks || pv != chk.n_private || fl != n_take)
+    return fail(EPIC_ERR_INVALID_ARG, "internal planner inconsistency (decode)");
+  return write_work(tiles, split, chk, plan);
 }

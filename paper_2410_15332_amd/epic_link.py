@@ -97,6 +97,12 @@ _plan_layout = _proto("epic_plan_layout", C.c_int, [_P(epic_plan_sizes), C.c_voi
 _plan_link = _proto("epic_plan_link", C.c_int,
                     [_P(epic_link_request), C.c_int32, _P(epic_attn_cfg), _i32p, C.c_int32, C.c_int32,
                      _P(epic_plan_sizes), _P(epic_plan)])
+_plan_decode_sizes = _proto("epic_plan_decode_sizes", C.c_int,
+                            [_P(epic_plan_sizes), _P(epic_plan), _i32p, _P(epic_attn_cfg), C.c_int32,
+                             _P(epic_plan_sizes)])
+_plan_decode = _proto("epic_plan_decode", C.c_int,
+                      [_P(epic_plan_sizes), _P(epic_plan), _i32p, _P(epic_attn_cfg), _i32p, C.c_int32, C.c_int32,
+                       _P(epic_plan_sizes), _P(epic_plan)])
 _link_ws = _proto("epic_link_workspace_bytes", C.c_size_t, [_P(epic_attn_cfg), _P(epic_plan_sizes)])
 _link_attention = _proto("epic_link_attention", C.c_int,
                          [_P(epic_attn_cfg), _P(epic_plan_sizes), _P(epic_plan), C.c_void_p, C.c_void_p,
@@ -120,7 +126,7 @@ _gemm = _proto("epic_gemm", C.c_int,
 EXPORTED = ["epic_status_string", "epic_last_error", "epic_version", "epic_plan_sizes_get", "epic_plan_layout",
             "epic_plan_link", "epic_link_workspace_bytes", "epic_link_attention", "epic_set_profile_events",
             "epic_model_workspace_bytes", "epic_link_layer", "epic_link_model", "epic_gemm_workspace_bytes",
-            "epic_gemm"]
+            "epic_gemm", "epic_plan_decode_sizes", "epic_plan_decode"]
 
 GEMM_STORE, GEMM_RESIDUAL, GEMM_SWIGLU = 0, 1, 2
 
@@ -195,6 +201,27 @@ def epic_plan_link(reqs: Sequence[Request], cfg: epic_attn_cfg, free_blocks: Seq
     plan = epic_plan_layout(sizes, buf.ctypes.data)
     _check(_plan_link(ra.arr, ra.n, C.byref(cfg), free.ctypes.data_as(_i32p), len(free), num_blocks,
                       C.byref(sizes), C.byref(plan)), "epic_plan_link")
+    return sizes, buf, plan_views(sizes, buf)
+
+
+def epic_plan_decode(prev_sizes: epic_plan_sizes, prev_buf: np.ndarray, new_tokens: Sequence[int],
+                     cfg: epic_attn_cfg, free_blocks: Sequence[int], num_blocks: int):
+    """Decode planner: append new_tokens[b] tokens to request b of the previous plan
+    (host buffer prev_buf of the link or a previous decode plan).  Returns (sizes,
+    host int32 buffer, numpy views) of the new plan."""
+    prev = epic_plan_layout(prev_sizes, prev_buf.ctypes.data)
+    nt = np.ascontiguousarray(new_tokens, np.int32)
+    if len(nt) != prev_sizes.batch:
+        raise ValueError("new_tokens needs one entry per request")
+    free = np.ascontiguousarray(free_blocks, np.int32)
+    sizes = epic_plan_sizes()
+    _check(_plan_decode_sizes(C.byref(prev_sizes), C.byref(prev), nt.ctypes.data_as(_i32p), C.byref(cfg), len(free),
+                              C.byref(sizes)), "epic_plan_decode_sizes")
+    buf = np.zeros(max(1, sizes.total_ints), np.int32)
+    plan = epic_plan_layout(sizes, buf.ctypes.data)
+    _check(_plan_decode(C.byref(prev_sizes), C.byref(prev), nt.ctypes.data_as(_i32p), C.byref(cfg),
+                        free.ctypes.data_as(_i32p), len(free), num_blocks, C.byref(sizes), C.byref(plan)),
+           "epic_plan_decode")
     return sizes, buf, plan_views(sizes, buf)
 
 

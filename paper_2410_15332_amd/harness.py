@@ -43,10 +43,59 @@ class AttnStage:
     out: object
     lse: object
     workspace: object
+    spare: List[int] = None                  # free blocks the link plan did not take
 
     def run(self, stream=None):
         el.epic_link_attention(self.cfg, self.dplan, self.q_s, self.k_s, self.v_s, self.k_cache, self.v_cache,
                                self.out, self.lse, self.workspace, stream)
+
+
+@dataclass
+class DecodeStage:
+    """One decode step after a link (or decode) plan: the new tokens' rows and plan."""
+    cfg: el.epic_attn_cfg
+    sizes: el.epic_plan_sizes
+    views: Dict[str, np.ndarray]
+    dplan: el.DevicePlan
+    spare: List[int]                         # free blocks left after this step
+    q_s: object
+    k_s: object
+    v_s: object
+    out: object
+    lse: object
+    workspace: object
+
+    def run(self, k_cache, v_cache, stream=None):
+        el.epic_link_attention(self.cfg, self.dplan, self.q_s, self.k_s, self.v_s, k_cache, v_cache,
+                               self.out, self.lse, self.workspace, stream)
+
+
+def stage_decode(wl: AttnWorkload, cfg: el.epic_attn_cfg, prev_sizes: el.epic_plan_sizes, prev_host: np.ndarray,
+                 spare: List[int], num_blocks: int, new_tokens: List[int], device="cuda") -> DecodeStage:
+    """Decode plan appending new_tokens[r] tokens to request r of the previous plan, with
+    the new tokens' q / k / v drawn by position like the link step's rows."""
+    import torch
+
+    hq, hkv, d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    sizes, host, views = el.epic_plan_decode(prev_sizes, prev_host, new_tokens, cfg, spare, num_blocks)
+    taken = sizes.n_linked_blocks - prev_sizes.n_linked_blocks
+    n_s = sizes.n_s
+    q = np.zeros((max(1, n_s), hq, d), np.uint16)
+    k = np.zeros((max(1, n_s), hkv, d), np.uint16)
+    v = np.zeros((max(1, n_s), hkv, d), np.uint16)
+    for r in range(sizes.batch):
+        a, b = int(views["s_off"][r]), int(views["s_off"][r + 1])
+        if b > a:
+            q[a:b], k[a:b], v[a:b] = synth.row_qkv(wl.seed, r, views["s_pos"][a:b], hq, hkv, d, wl.value_scale,
+                                                    wl.qk_scale)
+    ws_bytes = el.epic_link_workspace_bytes(cfg, sizes)
+    return DecodeStage(
+        cfg=cfg, sizes=sizes, views=views, dplan=el.DevicePlan(sizes, host, device), spare=list(spare[taken:]),
+        q_s=_bf16_tensor(q, device), k_s=_bf16_tensor(k, device), v_s=_bf16_tensor(v, device),
+        out=torch.zeros((max(1, n_s), hq, d), dtype=torch.bfloat16, device=device),
+        lse=torch.zeros((max(1, n_s), hq), dtype=torch.float32, device=device),
+        workspace=torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=device),
+    )
 
 
 def chunk_ids(wl: AttnWorkload) -> List[int]:
@@ -135,6 +184,7 @@ def stage_attention(wl: AttnWorkload, device="cuda", split_blocks: int = 0, spar
         out=torch.zeros((max(1, n_s), hq, d), dtype=torch.bfloat16, device=device),
         lse=torch.zeros((max(1, n_s), hq), dtype=torch.float32, device=device),
         workspace=torch.empty(max(256, ws_bytes), dtype=torch.uint8, device=device),
+        spare=[int(x) for x in free[sizes.n_private:]],
     )
 
 

@@ -363,3 +363,31 @@ def test_projection_brute_force():
     assert np.allclose(oracle.projection(a, w, "swiglu"), sw, rtol=0, atol=1e-12)
     # identity weights: the store epilogue returns the rows themselves
     assert np.array_equal(oracle.projection(a, np.eye(k), "store"), a)
+
+
+def test_decode_equals_link_of_the_grown_request():
+    """Decoding t tokens after a link step gives the rows the link step of the grown
+    request (its suffix t tokens longer, those t rows recomputed like every suffix
+    row) computes for them; and decoding 2 + 3 tokens in two steps gives the same as
+    5 at once (causal attention: earlier rows never see later keys)."""
+    rng = np.random.default_rng(11)
+    lens, suffix, k, hq, hkv, d = [9, 14, 7], 5, 3, 4, 2, 8
+    ck = [rng.standard_normal((L, hkv, d)) for L in lens]
+    cv = [rng.standard_normal((L, hkv, d)) for L in lens]
+    n_s = len(oracle.legolink_positions(lens, suffix, k))
+    t = 5
+    q = rng.standard_normal((n_s + t, hq, d))
+    kk = rng.standard_normal((n_s + t, hkv, d))
+    vv = rng.standard_normal((n_s + t, hkv, d))
+    pos, out, lse, K, V = oracle.decode_attention(lens, suffix, k, ck, cv, kk[:n_s], vv[:n_s],
+                                                  q[n_s:], kk[n_s:], vv[n_s:])
+    s_grown, out_g, lse_g, K_g, V_g = oracle.link_attention(lens, suffix + t, k, ck, cv, q, kk, vv)
+    assert np.array_equal(pos, s_grown[n_s:])
+    assert np.allclose(out, out_g[n_s:], rtol=0, atol=1e-12) and np.allclose(lse, lse_g[n_s:], rtol=0, atol=1e-12)
+    assert np.array_equal(K, K_g) and np.array_equal(V, V_g)
+    # two steps: 2 tokens, then 3 more after them
+    _, o1, _, _, _ = oracle.decode_attention(lens, suffix, k, ck, cv, kk[:n_s], vv[:n_s],
+                                             q[n_s:n_s + 2], kk[n_s:n_s + 2], vv[n_s:n_s + 2])
+    _, o2, _, _, _ = oracle.decode_attention(lens, suffix + 2, k, ck, cv, kk[:n_s + 2], vv[:n_s + 2],
+                                             q[n_s + 2:], kk[n_s + 2:], vv[n_s + 2:])
+    assert np.allclose(np.concatenate([o1, o2]), out, rtol=0, atol=1e-12)

@@ -219,3 +219,83 @@ def test_tile_rows_override_and_rejection():
     with pytest.raises(el.EpicError) as e:
         el.epic_plan_sizes_get(reqs, el.attn_cfg(32, 8, 128, 0.0, 0, 192), 1 << 30)
     assert e.value.status == 2
+
+
+
+def _check_linked(views, n_req):
+    """Linked tables: contiguous positions from 0; every S row's slot is the one its
+    position falls into."""
+    for r in range(n_req):
+        b0, b1 = views["blk_off"][r], views["blk_off"][r + 1]
+        pos0, blen = views["block_pos0"][b0:b1], views["block_len"][b0:b1]
+        if b1 > b0:
+            assert pos0[0] == 0 and np.all(pos0[1:] == pos0[:-1] + blen[:-1]) and np.all(blen >= 1)
+        for i in range(views["s_off"][r], views["s_off"][r + 1]):
+            p = int(views["s_pos"][i])
+            j = int(np.searchsorted(pos0, p, side="right") - 1)
+            assert pos0[j] <= p < pos0[j] + blen[j]
+            assert views["s_slot"][i] == views["linked_blocks"][b0 + j] * 16 + (p - pos0[j])
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_decode_plans_grow_the_link_plan(seed):
+    """Decode after the link step, twice: the previous linked table is kept (the last
+    block grows when the previous step wrote it), new blocks come from the free
+    list, S = the appended positions, and only blocks receiving a new token are
+    written (a block holding earlier tokens is its own copy source)."""
+    rng = np.random.default_rng(200 + seed)
+    reqs, n_used = _random_requests(rng, int(rng.integers(1, 5)), max_len=60)
+    cfg = el.attn_cfg(8, 2, 64)
+    need = el.epic_plan_sizes_get(reqs, cfg, 1 << 30).n_private
+    pool = n_used + need + 64
+    free = list(range(n_used, n_used + need))
+    sizes, buf, v = el.epic_plan_link(reqs, cfg, free, pool)
+    spare = list(range(n_used + need, pool))
+    for step in range(2):
+        new = [int(rng.integers(0, 20)) for _ in reqs]
+        ds, dbuf, d = el.epic_plan_decode(sizes, buf, new, cfg, spare, pool)
+        _check_linked(d, len(reqs))
+        written = set(v["priv_block"].tolist())
+        taken = 0
+        for r, t in enumerate(new):
+            a, e = v["blk_off"][r], v["blk_off"][r + 1]
+            c = d["blk_off"][r]
+            n = int(v["block_pos0"][e - 1] + v["block_len"][e - 1]) if e > a else 0
+            # previous blocks kept in place
+            assert np.array_equal(d["linked_blocks"][c:c + (e - a)], v["linked_blocks"][a:e])
+            assert np.array_equal(d["block_pos0"][c:c + (e - a)], v["block_pos0"][a:e])
+            room = 0
+            if e > a and v["block_len"][e - 1] < 16 and int(v["linked_blocks"][e - 1]) in written:
+                room = min(t, 16 - int(v["block_len"][e - 1]))
+            extra = -(-(t - room) // 16)
+            assert d["blk_off"][r + 1] - c == (e - a) + extra
+            assert d["linked_blocks"][c + (e - a):c + (e - a) + extra].tolist() == spare[taken:taken + extra]
+            taken += extra
+            s0, s1 = d["s_off"][r], d["s_off"][r + 1]
+            assert d["s_pos"][s0:s1].tolist() == list(range(n, n + t))
+        rows = d["priv_rows"].reshape(-1, 16)
+        for p in range(ds.n_private):
+            blk = int(d["priv_block"][p])
+            assert any(x >= 0 for x in rows[p]), "a listed block receives no new token"
+            assert d["priv_src"][p] == (blk if blk not in spare else -1)
+        assert sorted(x for x in rows.ravel().tolist() if x >= 0) == list(range(ds.n_s))
+        sizes, buf, v, spare = ds, dbuf, d, spare[taken:]
+
+
+def test_decode_after_a_suffix_free_link_starts_a_block():
+    """No suffix: the last linked block is a shared chunk block, never written, so the
+    first new token opens a new block even though the chunk block has free slots."""
+    cfg = el.attn_cfg(8, 8, 64)
+    sizes, buf, v = el.epic_plan_link([el.Request([20], [[0, 1]], 0, 4)], cfg, [], 8)
+    ds, _, d = el.epic_plan_decode(sizes, buf, [3], cfg, [5], 8)
+    assert d["linked_blocks"].tolist() == [0, 1, 5] and d["block_len"].tolist() == [16, 4, 3]
+    assert d["s_pos"].tolist() == [20, 21, 22] and d["priv_src"].tolist() == [-1]
+    with pytest.raises(el.EpicError) as e:                           # a linked block offered as free
+        el.epic_plan_decode(sizes, buf, [3], cfg, [1], 8)
+    assert e.value.status == 1
+    with pytest.raises(el.EpicError) as e:                           # free list too short
+        el.epic_plan_decode(sizes, buf, [40], cfg, [5, 6], 8)
+    assert e.value.status == 3
+    with pytest.raises(el.EpicError) as e:                           # negative count
+        el.epic_plan_decode(sizes, buf, [-1], cfg, [5], 8)
+    assert e.value.status == 1
