@@ -41,6 +41,10 @@ WORKLOADS = {
     "c2": ("c2", {}),
     "c1": ("c1", {}),
     "c3": ("c3", {}),
+    # compile step of the same 20 chunks with LegoLink-0's 4 dummy tokens, and the
+    # link step (k = 0) over those caches
+    "c3compile": ("c3", {}),
+    "c3lego0": ("c3", {"k": 0}),
     # decode after the link step (one new token per request), not the default line
     "c5k32dec": ("c5", {"k": 32}),
     "c4dec": ("c4", {}),
@@ -151,7 +155,107 @@ def cpu_baseline_model(wl, n_rows: int):
     }
 
 
-def bench_model(args, wl):
+def cpu_baseline_compile(wl, n_dummy: int, budget_s: float = 10.0):
+    """Time the float64 oracle's compile of one decoder layer, chunk after chunk
+    (each after the dummy tokens) until about budget_s seconds have passed; the
+    compile step is n_layers x that per compiled token."""
+    import numpy as np
+
+    import oracle
+    import synth
+    from threadpoolctl import threadpool_info
+
+    w = [synth.model_weights(wl.seed, 0, wl.hidden, wl.ffn, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, threads=8)]
+    fn = synth.final_norm_weight(wl.seed, wl.hidden)
+    dummy = synth.dummy_embeddings(wl.seed, n_dummy, wl.hidden).astype(np.float64) if n_dummy else None
+    dt, n_tok, n_chunks = 0.0, 0, 0
+    for j, L in enumerate(wl.chunk_lens):
+        emb = synth.token_embeddings(wl.seed, 0, j, range(L), wl.hidden).astype(np.float64)
+        t0 = time.perf_counter()
+        oracle.compile_chunk(emb, w, fn, wl.hidden, wl.ffn, wl.num_q_heads, wl.num_kv_heads, wl.head_dim,
+                             wl.rope_theta, wl.rms_eps, dummy_emb=dummy)
+        dt += time.perf_counter() - t0
+        n_tok += L
+        n_chunks += 1
+        if dt >= budget_s:
+            break
+    cores = max([x.get("num_threads", 1) for x in threadpool_info() if x.get("user_api") == "blas"] or [1])
+    return {
+        "value": round(n_tok / (dt * wl.n_layers), 4),
+        "unit": "compiled chunk tokens/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"1 of {wl.n_layers} decoder layers of {n_chunks} chunks x ({n_dummy} dummy + "
+                   f"{wl.chunk_lens[0]} tokens), float64 NumPy oracle, {dt:.1f} s; compile time = "
+                   f"{wl.n_layers} layers x that per token"),
+        "sample_seconds": round(dt, 2),
+    }
+
+
+def bench_compile(args, wl, n_dummy: int):
+    """Compile step of the 32-layer configuration: all chunks prefilled alone (each
+    after n_dummy dummy tokens, whose K/V are dropped), K/V stored per layer."""
+    import numpy as np
+    import torch
+
+    from paper_2410_15332_amd import epic_link as el
+    from paper_2410_15332_amd import harness
+
+    t0 = time.time()
+    st = harness.stage_model(wl, caches="compile", weights_on_device=True, n_dummy=n_dummy, keep_compile=True)
+    cst = st.compile_stage
+    torch.cuda.synchronize()
+    log(f"staged {wl.name}: compile n_s={cst.sizes.n_s} ({len(wl.chunk_lens)} chunks x ({n_dummy} + "
+        f"{wl.chunk_lens[0]})), {wl.n_layers} layers, in {time.time() - t0:.1f}s")
+    for _ in range(args.warmup):
+        cst.run(st.k_caches, st.v_caches)
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for e in (x for row in ev for x in row):
+        e.record()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(K):
+        el.epic_set_profile_events(ev[i])
+        cst.run(st.k_caches, st.v_caches)
+    end.record()
+    el.epic_set_profile_events(None)
+    torch.cuda.synchronize()
+    step_ms = start.elapsed_time(end) / K
+    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    n_s = cst.sizes.n_s
+    n_tok = sum(wl.chunk_lens)
+    attn_flops = harness.attention_flops(cst.views, wl.num_q_heads, wl.head_dim)
+    total = wl.n_layers * (attn_flops + harness.gemm_flops_per_layer(wl, n_s))
+    achieved = total / (step_ms * 1e-3) / 1e12
+    log(f"compile {step_ms:.3f} ms; layer attention {attn_ms:.4f} ms; all layers {achieved:.1f} TFLOP/s")
+    result = {
+        "metric": "compile step (ms) + compiled chunk tokens/s; whole-step TFLOP/s vs MFMA peak",
+        "value": round(n_tok / (step_ms * 1e-3), 1), "unit": "compiled chunk tokens/s", "n_gpus": 1,
+        "steps": K, "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (random-init weights, seeded N(0,1) token embeddings, one seeded dummy token)",
+        "config": {"workload": f"compile of {len(wl.chunk_lens)} x {wl.chunk_lens[0]} tokens + {n_dummy} dummy "
+                               f"tokens per chunk, {wl.n_layers}-layer Llama-3-8B shape",
+                   "layers": wl.n_layers, "hidden": wl.hidden, "ffn": wl.ffn, "num_q_heads": wl.num_q_heads,
+                   "num_kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim, "chunks": len(wl.chunk_lens),
+                   "chunk_len": wl.chunk_lens[0], "dummy_tokens": n_dummy, "rows": n_s,
+                   "parallelism": "single GPU"},
+        "attention_tflops": round(attn_flops / attn_ms / 1e9, 2),
+        "roofline": {"bound": "mfma", "kernel": "whole compile step (GEMMs + attention)",
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "algorithmic_flops_per_launch": total,
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on one decoder layer of one chunk ...")
+        result["cpu_baseline"] = cpu_baseline_compile(wl, n_dummy)
+    print(json.dumps(result), flush=True)
+
+
+def bench_model(args, wl, n_dummy: int = 0):
     """Full-model link step (all decoder layers + final norm) on the 32-layer configuration."""
     import numpy as np
     import torch
@@ -160,10 +264,10 @@ def bench_model(args, wl):
     from paper_2410_15332_amd import harness
 
     t0 = time.time()
-    st = harness.stage_model(wl, caches="compile", weights_on_device=True)
+    st = harness.stage_model(wl, caches="compile", weights_on_device=True, n_dummy=n_dummy)
     torch.cuda.synchronize()
     log(f"staged {wl.name}: n_s={st.sizes.n_s}, {wl.n_layers} layers, chunks compiled on the GPU "
-        f"in {time.time() - t0:.1f}s")
+        f"({n_dummy} dummy tokens) in {time.time() - t0:.1f}s")
     for _ in range(args.warmup):
         st.run()
     torch.cuda.synchronize()
@@ -197,7 +301,8 @@ def bench_model(args, wl):
         "config": {"workload": wl.name, "layers": wl.n_layers, "hidden": wl.hidden, "ffn": wl.ffn,
                    "num_q_heads": wl.num_q_heads, "num_kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim,
                    "chunks": len(wl.chunk_lens), "chunk_len": wl.chunk_lens[0], "suffix_len": wl.suffix_len,
-                   "k": wl.k, "recomputed_rows": n_s, "linked_tokens": int(st.sizes.max_pos),
+                   "k": wl.k, "compile_dummy_tokens": n_dummy, "recomputed_rows": n_s,
+                   "linked_tokens": int(st.sizes.max_pos),
                    "parallelism": "single GPU"},
         "ttft_ms": round(step_ms, 4),
         "attention_tflops": round(attn_flops / attn_ms / 1e9, 2),
@@ -293,8 +398,11 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     name, kw = WORKLOADS[args.workload]
     wl = get_config(name, **kw)
+    if args.workload == "c3compile":
+        bench_compile(args, wl, 4)
+        return
     if name == "c3":
-        bench_model(args, wl)
+        bench_model(args, wl, 4 if args.workload == "c3lego0" else 0)
         return
     if args.workload.endswith("dec"):
         bench_decode(args, wl)

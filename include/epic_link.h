@@ -178,6 +178,39 @@ epic_status epic_plan_decode(const epic_plan_sizes* prev_sizes, const epic_plan*
                              const epic_attn_cfg* cfg, const int32_t* free_blocks, int32_t n_free,
                              int32_t num_blocks, const epic_plan_sizes* sizes, epic_plan* plan);
 
+/* Compile step (Sec. 2.2): every chunk is prefilled alone, positions from 0, and
+ * its K/V per layer become the chunk's cache.  LegoLink-0 (Sec. 5.4) prepends
+ * n_dummy dummy tokens to every chunk for this prefill and drops their K/V, so
+ * the cache holds the chunk's L tokens only (token t at block t / bs, offset
+ * t % bs), rotated at their compile positions n_dummy + t.
+ * chunk_blocks[chunk_block_off[j] .. chunk_block_off[j+1]): the ceil(L_j / bs)
+ * blocks that receive chunk j's cache (all distinct).  n_dummy >= 0. */
+typedef struct {
+  int32_t num_chunks;
+  const int32_t* chunk_len;        /* [num_chunks], each >= 1 */
+  const int32_t* chunk_block_off;  /* [num_chunks + 1], CSR offsets, [0] == 0 */
+  const int32_t* chunk_blocks;     /* physical block ids receiving the caches */
+  int32_t n_dummy;                 /* dummy tokens prepended to every chunk (0 = plain compile) */
+} epic_compile_batch;
+
+/* Host only, integer, synchronous.  The compile plan has one request per chunk,
+ * in order: S = its n_dummy + L_j tokens at positions 0 .. n_dummy + L_j - 1, the
+ * dummies first, so the caller's S rows (hidden states) of chunk j are n_dummy
+ * dummy rows then the chunk's L_j token rows.  With n_dummy == 0 the linked
+ * blocks are the chunk blocks and free_blocks is not used.  With n_dummy > 0
+ * the attention reads the n_dummy + L_j tokens from ceil((n_dummy + L_j) / bs)
+ * staging blocks per chunk taken in order from free_blocks (distinct, not chunk
+ * blocks; EPIC_ERR_NO_PRIVATE_BLOCKS if too few), and the chunk blocks are
+ * private blocks outside the linked table that receive rows n_dummy .. (the
+ * staging blocks hold the dummy-inclusive K/V afterwards and may be reused).
+ * epic_link_model (or epic_link_attention per layer) with this plan is the
+ * compile step; s_slot gives the linked (staging) slot of every row. */
+epic_status epic_plan_compile_sizes(const epic_compile_batch* batch, const epic_attn_cfg* cfg, int32_t n_free,
+                                    epic_plan_sizes* out);
+epic_status epic_plan_compile(const epic_compile_batch* batch, const epic_attn_cfg* cfg,
+                              const int32_t* free_blocks, int32_t n_free, int32_t num_blocks,
+                              const epic_plan_sizes* sizes, epic_plan* plan);
+
 /* Workspace bytes epic_link_attention needs for this plan (split-KV partials). */
 size_t epic_link_workspace_bytes(const epic_attn_cfg* cfg, const epic_plan_sizes* sizes);
 

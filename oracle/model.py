@@ -10,7 +10,8 @@ inverse frequencies theta^(-2i/d), grouped-query attention, SwiGLU MLP, final
 RMSNorm.  No LM head (the link step ends at the last hidden state).
 
 The compile step (Sec. 2.2) runs one chunk alone through the same model with
-positions 0..L-1 and keeps each layer's K and V.
+positions 0..L-1 and keeps each layer's K and V; LegoLink-0 (Sec. 5.4) runs
+dummy tokens plus the chunk and keeps the chunk's K and V only.
 
 Precision reading: weights, KV caches and the activations fed to a weight
 matrix are bf16; everything else is float64 here.  With ``bf16_storage`` the
@@ -140,13 +141,22 @@ def link_model(emb_s: np.ndarray, chunk_lens: Sequence[int], suffix_len: int, k:
 
 def compile_chunk(emb_chunk: np.ndarray, weights: Sequence[Dict[str, np.ndarray]],
                   final_norm: np.ndarray, hidden: int, ffn: int, hq: int, hkv: int, d: int,
-                  theta: float, eps: float, bf16_storage: bool = True):
+                  theta: float, eps: float, bf16_storage: bool = True, dummy_emb: np.ndarray = None):
     """Compile step (Sec. 2.2): prefill one chunk alone at positions 0..L-1.
 
     This is the link step of a request with no cached chunks whose tokens are
     all new, so every token is computed.  Returns (hidden out, per-layer (K, V)).
+
+    dummy_emb [n_dummy, hidden]: LegoLink-0's compile (Sec. 5.4).  The dummy
+    tokens are placed before the chunk, the n_dummy + L tokens are prefilled
+    together at positions 0..n_dummy+L-1, and the dummies' rows are then
+    dropped: the returned hidden states and K/V are the chunk's L rows only,
+    their K rotated at positions n_dummy..n_dummy+L-1.
     """
-    L = emb_chunk.shape[0]
-    _, out, kv = link_model(emb_chunk, [], L, 0, weights, final_norm, [([], [])] * len(weights),
+    nd = 0 if dummy_emb is None else int(np.asarray(dummy_emb).shape[0])
+    rows = emb_chunk if nd == 0 else np.concatenate([np.asarray(dummy_emb, np.float64),
+                                                     np.asarray(emb_chunk, np.float64)])
+    n = rows.shape[0]
+    _, out, kv = link_model(rows, [], n, 0, weights, final_norm, [([], [])] * len(weights),
                             hidden, ffn, hq, hkv, d, theta, eps, bf16_storage)
-    return out, kv
+    return out[nd:], [(k[nd:], v[nd:]) for k, v in kv]

@@ -680,3 +680,150 @@ extern "C" epic_status epic_plan_decode(const epic_plan_sizes* prev_sizes, const
     return fail(EPIC_ERR_INVALID_ARG, "internal planner inconsistency (decode)");
   return write_work(tiles, split, chk, plan);
 }
+
+// ---------------------------------------------------------------- compile
+
+namespace {
+
+// The compile step (Sec. 2.2) prefills every chunk alone; LegoLink-0 (Sec. 5.4)
+// first prepends n_dummy dummy tokens to each chunk and afterwards drops their
+// K/V.  Each chunk is one request of the plan: S = its n_dummy + L tokens at
+// positions 0 .. n_dummy + L - 1, the dummies first.  Without dummies the
+// chunk's own blocks are its linked (attention) blocks.  With dummies the
+// attention reads n_dummy + L tokens from staging blocks taken from the free
+// list, and the chunk's blocks are further private blocks outside the linked
+// table that receive chunk token t at slot t (rows n_dummy + t).
+epic_status compile_shape(const epic_compile_batch* cb, const epic_attn_cfg* cfg, int32_t n_free,
+                          epic_plan_sizes* out, std::vector<Tile>* tiles_out, int* split_out,
+                          int64_t* n_staging) {
+  EPIC_CHECK_ARG(cb && out, "NULL compile batch or output sizes");
+  EPIC_CHECK_ARG(n_free >= 0, "n_free %d < 0", n_free);
+  epic_status st = validate_attn_cfg(cfg);
+  if (st != EPIC_OK) return st;
+  const int n = cb->num_chunks;
+  EPIC_CHECK_ARG(n >= 0, "num_chunks %d < 0", n);
+  EPIC_CHECK_ARG(cb->n_dummy >= 0 && cb->n_dummy <= (1 << 20), "n_dummy %d outside [0, 2^20]", cb->n_dummy);
+  if (n > 0) {
+    EPIC_CHECK_ARG(cb->chunk_len && cb->chunk_block_off && cb->chunk_blocks, "chunk arrays are NULL");
+    EPIC_CHECK_ARG(cb->chunk_block_off[0] == 0, "chunk_block_off[0] != 0");
+  }
+  const int nd = cb->n_dummy;
+  std::vector<ReqRows> rr(static_cast<size_t>(n));
+  int64_t n_s = 0, n_lb = 0, n_priv = 0, stage = 0, max_pos = 0;
+  for (int j = 0; j < n; ++j) {
+    const int L = cb->chunk_len[j];
+    EPIC_CHECK_ARG(L >= 1, "chunk %d: length %d < 1", j, L);
+    EPIC_CHECK_ARG(int64_t(L) + nd < (int64_t(1) << 30), "chunk %d: too many tokens", j);
+    const int nb = cb->chunk_block_off[j + 1] - cb->chunk_block_off[j];
+    EPIC_CHECK_ARG(nb == cdiv(L, kBlock), "chunk %d: %d blocks given, %d needed", j, nb, cdiv(L, kBlock));
+    const int total = nd + L, lb = cdiv(total, kBlock);
+    for (int p = 0; p < total; ++p) rr[j].pos.push_back(p);
+    for (int i = 0; i < lb; ++i) rr[j].p0.push_back(i * kBlock);
+    n_s += total;
+    n_lb += lb;
+    n_priv += nb + (nd > 0 ? lb : 0);
+    stage += nd > 0 ? lb : 0;
+    max_pos = std::max<int64_t>(max_pos, total);
+  }
+  EPIC_CHECK_ARG(n_s < (int64_t(1) << 30) && n_priv < (int64_t(1) << 30), "batch too large");
+  if (stage > n_free)
+    return fail(EPIC_ERR_NO_PRIVATE_BLOCKS, "plan needs %lld staging blocks, %d free", (long long)stage, n_free);
+  epic_plan_sizes s{};
+  s.batch = n;
+  choose_tiles(rr, cfg, &s, tiles_out, split_out);
+  s.n_s = static_cast<int32_t>(n_s);
+  s.n_linked_blocks = static_cast<int32_t>(n_lb);
+  s.n_private = static_cast<int32_t>(n_priv);
+  s.max_pos = static_cast<int32_t>(max_pos);
+  finish_sizes(&s);
+  *out = s;
+  *n_staging = stage;
+  return EPIC_OK;
+}
+
+}  // namespace
+
+extern "C" epic_status epic_plan_compile_sizes(const epic_compile_batch* batch, const epic_attn_cfg* cfg,
+                                               int32_t n_free, epic_plan_sizes* out) {
+  clear_error();
+  std::vector<Tile> tiles;
+  int split = 0;
+  int64_t stage = 0;
+  return compile_shape(batch, cfg, n_free, out, &tiles, &split, &stage);
+}
+
+extern "C" epic_status epic_plan_compile(const epic_compile_batch* batch, const epic_attn_cfg* cfg,
+                                         const int32_t* free_blocks, int32_t n_free, int32_t num_blocks,
+                                         const epic_plan_sizes* sizes, epic_plan* plan) {
+  clear_error();
+  epic_plan_sizes chk;
+  std::vector<Tile> tiles;
+  int split = 0;
+  int64_t stage = 0;
+  epic_status st = compile_shape(batch, cfg, n_free, &chk, &tiles, &split, &stage);
+  if (st != EPIC_OK) return st;
+  EPIC_CHECK_ARG(sizes && plan, "NULL sizes or plan");
+  EPIC_CHECK_ARG(std::memcmp(&chk, sizes, sizeof(chk)) == 0, "sizes do not match this compile batch");
+  EPIC_CHECK_ARG(num_blocks > 0, "num_blocks %d <= 0", num_blocks);
+  EPIC_CHECK_ARG(stage == 0 || free_blocks != nullptr, "free_blocks is NULL");
+  const int n = batch->num_chunks, nd = batch->n_dummy, bs = kBlock;
+  // every block is written: chunk blocks and staging blocks in range and all distinct
+  std::vector<uint8_t> used(static_cast<size_t>(num_blocks), 0);
+  const int n_chunk_blocks = n > 0 ? batch->chunk_block_off[n] : 0;
+  for (int i = 0; i < n_chunk_blocks; ++i) {
+    const int id = batch->chunk_blocks[i];
+    EPIC_CHECK_ARG(id >= 0 && id < num_blocks, "chunk block id %d out of range [0, %d)", id, num_blocks);
+    EPIC_CHECK_ARG(used[id] == 0, "chunk block %d is listed twice", id);
+    used[id] = 1;
+  }
+  for (int64_t i = 0; i < stage; ++i) {
+    const int id = free_blocks[i];
+    EPIC_CHECK_ARG(id >= 0 && id < num_blocks, "free block id %d out of range [0, %d)", id, num_blocks);
+    EPIC_CHECK_ARG(used[id] == 0, "free block %d is a chunk block or listed twice", id);
+    used[id] = 2;
+  }
+  int row = 0, lb = 0, pv = 0, fl = 0;
+  for (int j = 0; j < n; ++j) {
+    const int L = batch->chunk_len[j], total = nd + L;
+    const int32_t* cbk = batch->chunk_blocks + batch->chunk_block_off[j];
+    const int row0 = row;
+    plan->s_off[j] = row;
+    plan->blk_off[j] = lb;
+    // linked (attention) blocks: the chunk's own blocks, or staging blocks with dummies
+    for (int i = 0; i * bs < total; ++i, ++lb, ++pv) {
+      const int id = nd > 0 ? free_blocks[fl++] : cbk[i];
+      const int len = std::min(bs, total - i * bs);
+      plan->linked_blocks[lb] = id;
+      plan->block_pos0[lb] = i * bs;
+      plan->block_len[lb] = len;
+      plan->priv_block[pv] = id;
+      plan->priv_src[pv] = -1;
+      for (int o = 0; o < bs; ++o) {
+        int32_t r = -1;
+        if (o < len) {
+          r = row++;
+          plan->s_pos[r] = i * bs + o;
+          plan->s_req[r] = j;
+          plan->s_slot[r] = id * bs + o;
+        }
+        plan->priv_rows[int64_t(pv) * bs + o] = r;
+      }
+    }
+    // the chunk's cache without the dummies: chunk token t (row row0 + nd + t) at slot t
+    if (nd > 0) {
+      for (int i = 0; i * bs < L; ++i, ++pv) {
+        plan->priv_block[pv] = cbk[i];
+        plan->priv_src[pv] = -1;
+        for (int o = 0; o < bs; ++o) {
+          const int t = i * bs + o;
+          plan->priv_rows[int64_t(pv) * bs + o] = t < L ? row0 + nd + t : -1;
+        }
+      }
+    }
+  }
+  plan->s_off[n] = row;
+  plan->blk_off[n] = lb;
+  if (row != chk.n_s || lb != chk.n_linked_blocks || pv != chk.n_private || fl != stage)
+    return fail(EPIC_ERR_INVALID_ARG, "internal planner inconsistency (compile)");
+  return write_work(tiles, split, chk, plan);
+}

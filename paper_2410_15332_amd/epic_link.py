@@ -56,6 +56,11 @@ class epic_link_request(C.Structure):
                 ("chunk_blocks", _i32p), ("suffix_len", C.c_int32), ("k", C.c_int32)]
 
 
+class epic_compile_batch(C.Structure):
+    _fields_ = [("num_chunks", C.c_int32), ("chunk_len", _i32p), ("chunk_block_off", _i32p),
+                ("chunk_blocks", _i32p), ("n_dummy", C.c_int32)]
+
+
 class epic_plan_sizes(C.Structure):
     _fields_ = [("batch", C.c_int32), ("n_s", C.c_int32), ("n_linked_blocks", C.c_int32),
                 ("n_private", C.c_int32), ("n_tiles", C.c_int32), ("n_work", C.c_int32),
@@ -103,6 +108,11 @@ _plan_decode_sizes = _proto("epic_plan_decode_sizes", C.c_int,
 _plan_decode = _proto("epic_plan_decode", C.c_int,
                       [_P(epic_plan_sizes), _P(epic_plan), _i32p, _P(epic_attn_cfg), _i32p, C.c_int32, C.c_int32,
                        _P(epic_plan_sizes), _P(epic_plan)])
+_plan_compile_sizes = _proto("epic_plan_compile_sizes", C.c_int,
+                             [_P(epic_compile_batch), _P(epic_attn_cfg), C.c_int32, _P(epic_plan_sizes)])
+_plan_compile = _proto("epic_plan_compile", C.c_int,
+                       [_P(epic_compile_batch), _P(epic_attn_cfg), _i32p, C.c_int32, C.c_int32,
+                        _P(epic_plan_sizes), _P(epic_plan)])
 _link_ws = _proto("epic_link_workspace_bytes", C.c_size_t, [_P(epic_attn_cfg), _P(epic_plan_sizes)])
 _link_attention = _proto("epic_link_attention", C.c_int,
                          [_P(epic_attn_cfg), _P(epic_plan_sizes), _P(epic_plan), C.c_void_p, C.c_void_p,
@@ -126,7 +136,8 @@ _gemm = _proto("epic_gemm", C.c_int,
 EXPORTED = ["epic_status_string", "epic_last_error", "epic_version", "epic_plan_sizes_get", "epic_plan_layout",
             "epic_plan_link", "epic_link_workspace_bytes", "epic_link_attention", "epic_set_profile_events",
             "epic_model_workspace_bytes", "epic_link_layer", "epic_link_model", "epic_gemm_workspace_bytes",
-            "epic_gemm", "epic_plan_decode_sizes", "epic_plan_decode"]
+            "epic_gemm", "epic_plan_decode_sizes", "epic_plan_decode", "epic_plan_compile_sizes",
+            "epic_plan_compile"]
 
 GEMM_STORE, GEMM_RESIDUAL, GEMM_SWIGLU = 0, 1, 2
 
@@ -222,6 +233,29 @@ def epic_plan_decode(prev_sizes: epic_plan_sizes, prev_buf: np.ndarray, new_toke
     _check(_plan_decode(C.byref(prev_sizes), C.byref(prev), nt.ctypes.data_as(_i32p), C.byref(cfg),
                         free.ctypes.data_as(_i32p), len(free), num_blocks, C.byref(sizes), C.byref(plan)),
            "epic_plan_decode")
+    return sizes, buf, plan_views(sizes, buf)
+
+
+def epic_plan_compile(chunk_lens: Sequence[int], chunk_blocks: Sequence[Sequence[int]], n_dummy: int,
+                      cfg: epic_attn_cfg, free_blocks: Sequence[int], num_blocks: int):
+    """Compile planner: one request per chunk, S = n_dummy dummy tokens then the
+    chunk's tokens; chunk_blocks[j] receive chunk j's cache (dummies dropped);
+    with n_dummy > 0 the attention stages through blocks taken from free_blocks.
+    Returns (sizes, host int32 buffer, numpy views)."""
+    lens = np.ascontiguousarray(chunk_lens, np.int32)
+    off = np.zeros(len(lens) + 1, np.int32)
+    off[1:] = np.cumsum([len(b) for b in chunk_blocks])
+    blocks = np.asarray([x for b in chunk_blocks for x in b] or [0], np.int32)
+    cb = epic_compile_batch(len(lens), lens.ctypes.data_as(_i32p), off.ctypes.data_as(_i32p),
+                            blocks.ctypes.data_as(_i32p), n_dummy)
+    free = np.ascontiguousarray(free_blocks if len(free_blocks) else [0], np.int32)
+    n_free = len(free_blocks)
+    sizes = epic_plan_sizes()
+    _check(_plan_compile_sizes(C.byref(cb), C.byref(cfg), n_free, C.byref(sizes)), "epic_plan_compile_sizes")
+    buf = np.zeros(max(1, sizes.total_ints), np.int32)
+    plan = epic_plan_layout(sizes, buf.ctypes.data)
+    _check(_plan_compile(C.byref(cb), C.byref(cfg), free.ctypes.data_as(_i32p), n_free, num_blocks,
+                         C.byref(sizes), C.byref(plan)), "epic_plan_compile")
     return sizes, buf, plan_views(sizes, buf)
 
 

@@ -213,6 +213,7 @@ class ModelStage:
     hidden: object                           # torch fp32 [n_s, hidden], overwritten by a run
     out: object                              # torch fp32 [n_s, hidden]
     workspace: object
+    compile_stage: object = None             # kept with keep_compile=True (its out: compiled hidden rows)
 
     def run(self, stream=None):
         self.hidden.copy_(self.emb)
@@ -257,12 +258,60 @@ def _device_weights(wl, layer: int, device):
             "w_gate_up": lin(2 * F, H), "w_down": lin(H, F)}
 
 
+@dataclass
+class CompileStage:
+    """Compile step of a model-level workload: every chunk prefilled alone (after
+    n_dummy dummy tokens for LegoLink-0), its K/V stored into its chunk blocks."""
+
+    cfg: el.epic_model_cfg
+    layers: List[el.epic_layer_weights]
+    final_norm: object
+    sizes: el.epic_plan_sizes
+    views: Dict[str, np.ndarray]
+    dplan: el.DevicePlan
+    emb: object                              # torch fp32 [n_s, hidden]: per chunk, dummies then tokens
+    hidden: object
+    out: object
+    workspace: object
+
+    def run(self, k_caches, v_caches, stream=None):
+        self.hidden.copy_(self.emb)
+        el.epic_link_model(self.cfg, self.layers, self.final_norm, self.dplan, self.hidden, k_caches, v_caches,
+                           self.out, self.workspace, stream)
+
+
+def compile_rows(wl, n_dummy: int) -> np.ndarray:
+    """Layer-0 rows of the compile plan: for every chunk, n_dummy dummy rows, then its tokens."""
+    H = wl.hidden
+    dummy = synth.dummy_embeddings(wl.seed, n_dummy, H)
+    parts = []
+    for j, n in enumerate(wl.chunk_lens):
+        if n_dummy:
+            parts.append(dummy)
+        parts.append(synth.token_embeddings(wl.seed, 0, j, range(n), H))
+    return np.concatenate(parts)
+
+
+def stage_compile(wl, cfg, layers, final_norm, chunk_blocks, free, num_blocks, n_dummy, device="cuda"):
+    import torch
+
+    csizes, chost, _ = el.epic_plan_compile(list(wl.chunk_lens), chunk_blocks, n_dummy, cfg.attn, free, num_blocks)
+    cplan = el.DevicePlan(csizes, chost, device)
+    h = torch.from_numpy(compile_rows(wl, n_dummy)).to(device)
+    ws = torch.empty(max(256, el.epic_model_workspace_bytes(cfg, csizes)), dtype=torch.uint8, device=device)
+    return CompileStage(cfg=cfg, layers=layers, final_norm=final_norm, sizes=csizes,
+                        views=el.plan_views(csizes, chost), dplan=cplan, emb=h, hidden=torch.empty_like(h),
+                        out=torch.empty_like(h), workspace=ws)
+
+
 def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: float = 0.5, device="cuda",
-                threads: int = 8, weights_on_device: bool = False) -> ModelStage:
+                threads: int = 8, weights_on_device: bool = False, n_dummy: int = 0,
+                keep_compile: bool = False) -> ModelStage:
     """Weights, per-chunk caches, link plan and S-row embeddings for a model-level workload.
 
-    caches="compile": every chunk is compiled on the GPU by the library itself (a
-    request with no cached chunks whose suffix is the chunk, positions 0..L-1);
+    caches="compile": every chunk is compiled on the GPU by the library itself
+    (epic_plan_compile + epic_link_model, positions 0..L-1; with n_dummy > 0,
+    LegoLink-0's compile: n_dummy copies of one dummy token first, dropped after);
     caches="synthetic": every layer's chunk caches are seeded N(0, cache_scale^2) draws.
     weights_on_device: draw the weights with a seeded device generator (timing runs)
     instead of synth.model_weights (parity runs).
@@ -289,7 +338,9 @@ def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: 
     nb = [-(-x // el.BLOCK) for x in wl.chunk_lens]
     link_req0 = el.Request(list(wl.chunk_lens), [[0] * n for n in nb], wl.suffix_len, wl.k)
     n_priv = el.epic_plan_sizes_get([link_req0], acfg, 1 << 30).n_private
-    num_blocks = sum(nb) + n_priv
+    # staging blocks of a dummy-token compile; free again once the compile is done
+    n_stage = sum(-(-(n_dummy + x) // el.BLOCK) for x in wl.chunk_lens) if n_dummy > 0 else 0
+    num_blocks = sum(nb) + max(n_priv, n_stage, 1)
     perm = np.random.default_rng([wl.seed, 99]).permutation(num_blocks).astype(np.int32)
     chunk_blocks, nxt = [], 0
     for n in nb:
@@ -300,20 +351,11 @@ def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: 
     v_caches = [torch.zeros((num_blocks, hkv, d, el.BLOCK), dtype=torch.bfloat16, device=device) for _ in range(L)]
 
     if caches == "compile" and m > 0:
-        # one request per chunk: no cached chunks, the chunk's tokens as new suffix tokens
-        creqs = [el.Request([], [], n_tok, 0) for n_tok in wl.chunk_lens]
-        cfree = [b for blocks in chunk_blocks for b in blocks]
-        csizes, chost, cviews = el.epic_plan_link(creqs, acfg, cfree, num_blocks)
-        assert cviews["priv_block"].tolist() == cfree
-        cplan = el.DevicePlan(csizes, chost, device)
-        emb = np.concatenate([synth.token_embeddings(wl.seed, 0, j, range(n), H)
-                              for j, n in enumerate(wl.chunk_lens)])
-        h = torch.from_numpy(emb).to(device)
-        out = torch.empty_like(h)
-        ws = torch.empty(max(256, el.epic_model_workspace_bytes(cfg, csizes)), dtype=torch.uint8, device=device)
-        el.epic_link_model(cfg, layers, final_norm, cplan, h, k_caches, v_caches, out, ws)
+        cst = stage_compile(wl, cfg, layers, final_norm, chunk_blocks, free, num_blocks, n_dummy, device)
+        cst.run(k_caches, v_caches)
         torch.cuda.synchronize()
-        del h, out, ws
+        if not keep_compile:
+            cst = None
     elif caches == "synthetic":
         for layer in range(L):
             kp = np.zeros((num_blocks, hkv, el.BLOCK, d), np.uint16)
@@ -335,7 +377,7 @@ def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: 
     return ModelStage(wl=wl, cfg=cfg, weights=weights, layers=layers, final_norm=final_norm, k_caches=k_caches,
                       v_caches=v_caches, requests=[req], chunk_block_ids=chunk_blocks, sizes=sizes, views=views,
                       dplan=dplan, emb=emb_t, hidden=torch.empty_like(emb_t), out=torch.empty_like(emb_t),
-                      workspace=ws)
+                      workspace=ws, compile_stage=cst if caches == "compile" and m > 0 else None)
 
 
 def gemm_flops_per_layer(wl, n_rows: int) -> float:

@@ -13,6 +13,7 @@ from .gen import (  # noqa: F401
     model_weights,
     final_norm_weight,
     token_embeddings,
+    dummy_embeddings,
     matrix_bf16,
     matrix_f32,
 )

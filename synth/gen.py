@@ -11,7 +11,8 @@ Identities:
   * recomputed row: (seed, "row", request, linked position) -> q [Hq, D], k, v [Hkv, D]
   * token         : (seed, "tok", kind, owner, index) -> embedding [hidden] (fp32)
                     kind 0 = token ``index`` of chunk ``owner``,
-                    kind 1 = suffix token ``index`` of request ``owner``
+                    kind 1 = suffix token ``index`` of request ``owner``,
+                    kind 2 = the dummy token (owner 0, index 0)
   * weights       : (seed, "w", layer, tensor id)
 """
 from __future__ import annotations
@@ -76,6 +77,14 @@ def token_embeddings(seed: int, kind: int, owner: int, indices: Sequence[int], h
         rng = np.random.default_rng([seed, _TOK, kind, owner, int(t)])
         out[i] = rng.standard_normal(size=hidden, dtype=np.float32)
     return out
+
+
+def dummy_embeddings(seed: int, n_dummy: int, hidden: int) -> np.ndarray:
+    """fp32 [n_dummy, hidden]: n_dummy copies of one dummy token's embedding (a
+    begin-of-sequence-like token prepended to every chunk at compile)."""
+    if n_dummy <= 0:
+        return np.zeros((0, hidden), np.float32)
+    return np.repeat(token_embeddings(seed, 2, 0, [0], hidden), n_dummy, axis=0)
 
 
 # tensor ids inside one layer

@@ -91,17 +91,36 @@ def _check(st, n_layers, caches_ref):
     return err
 
 
-def _oracle_compiled_caches(wl, n_layers):
+def _oracle_compiled_caches(wl, n_layers, n_dummy=0, outs=None):
     ws, fn = _oracle_inputs(wl, n_layers)
+    dummy = synth.dummy_embeddings(wl.seed, n_dummy, wl.hidden).astype(np.float64) if n_dummy else None
     ck = [[] for _ in range(n_layers)]
     cv = [[] for _ in range(n_layers)]
     for j, L in enumerate(wl.chunk_lens):
         emb = synth.token_embeddings(wl.seed, 0, j, range(L), wl.hidden).astype(np.float64)
-        _, kv = oracle.compile_chunk(emb, ws, fn, bf16_storage=True, **_dims(wl))
+        out, kv = oracle.compile_chunk(emb, ws, fn, bf16_storage=True, dummy_emb=dummy, **_dims(wl))
+        if outs is not None:
+            outs.append(out)
         for layer, (k, v) in enumerate(kv):
             ck[layer].append(k)
             cv[layer].append(v)
     return list(zip(ck, cv))
+
+
+def _check_chunk_caches(st, ref):
+    """The chunk blocks hold each chunk's compiled K/V, token t at slot t."""
+    wl = st.wl
+    for layer in range(wl.n_layers):
+        kc, vc = _bits(st.k_caches[layer]), _bits(st.v_caches[layer])
+        for j, blocks in enumerate(st.chunk_block_ids):
+            L = wl.chunk_lens[j]
+            kb = kc[blocks].transpose(0, 2, 1, 3).reshape(-1, wl.num_kv_heads, wl.head_dim)
+            vb = vc[blocks].transpose(0, 3, 1, 2).reshape(-1, wl.num_kv_heads, wl.head_dim)
+            ek = np.abs(_f64(kb[:L]) - ref[layer][0][j]).max()
+            ev = np.abs(_f64(vb[:L]) - ref[layer][1][j]).max()
+            assert ek <= ATOL and ev <= ATOL, f"layer {layer} chunk {j}: compiled K/V err {ek}, {ev}"
+            # slots past the chunk's end are zero (nothing of the dummies or a neighbour leaks in)
+            assert not kb[L:].any() and not vb[L:].any(), f"layer {layer} chunk {j}: stray rows"
 
 
 def _small(name, lens, suffix, k, hidden=512, ffn=1024, hq=8, hkv=2, d=64, layers=3, seed=31):
@@ -123,16 +142,36 @@ def test_compile_and_link_small(wl):
     torch.cuda.synchronize()
     # the GPU-compiled chunk caches against the oracle's compile (bf16 data, tolerance)
     ref = _oracle_compiled_caches(wl, wl.n_layers)
-    from paper_2410_15332_amd import epic_link as el
-    for layer in range(wl.n_layers):
-        kc, vc = _bits(st.k_caches[layer]), _bits(st.v_caches[layer])
-        for j, blocks in enumerate(st.chunk_block_ids):
-            L = wl.chunk_lens[j]
-            kb = kc[blocks].transpose(0, 2, 1, 3).reshape(-1, wl.num_kv_heads, wl.head_dim)[:L]
-            vb = vc[blocks].transpose(0, 3, 1, 2).reshape(-1, wl.num_kv_heads, wl.head_dim)[:L]
-            assert np.abs(_f64(kb) - ref[layer][0][j]).max() <= ATOL
-            assert np.abs(_f64(vb) - ref[layer][1][j]).max() <= ATOL
+    _check_chunk_caches(st, ref)
     _check(st, wl.n_layers, ref)
+
+
+LEGO0 = [
+    (_small("lego0_ragged_d64", [37, 100, 16, 51, 12], 23, 0), 4),
+    (_small("lego0_d128_g2", [64, 45, 80], 30, 0, hidden=512, ffn=1536, hq=4, hkv=2, d=128), 4),
+    (_small("dummy_block_k3", [20, 28], 9, 3, layers=2), 16),
+]
+
+
+@pytest.mark.parametrize("wl,nd", LEGO0, ids=[f"{w.name}_nd{n}" for w, n in LEGO0])
+def test_dummy_compile_then_link(wl, nd):
+    """LegoLink-0 (Sec. 5.4): each side compiles every chunk after nd dummy tokens
+    and drops their K/V; the GPU's chunk caches and compiled hidden rows match the
+    oracle's, then the link step over those caches (k = 0: only the suffix is
+    computed) matches end to end."""
+    st = _stage(wl, caches="compile", n_dummy=nd, keep_compile=True)
+    outs = []
+    ref = _oracle_compiled_caches(wl, wl.n_layers, nd, outs)
+    _check_chunk_caches(st, ref)
+    cst = st.compile_stage
+    got = cst.out.double().cpu().numpy()
+    for j, L in enumerate(wl.chunk_lens):
+        a = int(cst.views["s_off"][j])
+        err = np.abs(got[a + nd:a + nd + L] - outs[j]).max()
+        assert err <= ATOL, f"chunk {j}: compiled hidden max |err| {err}"
+    st.run()
+    err = _check(st, wl.n_layers, ref)
+    print(f"[gpu-test] {wl.name} nd={nd}: linked final hidden max|err| {err:.3e}", flush=True)
 
 
 def test_recompute_all_equals_full_prefill():

@@ -391,3 +391,50 @@ def test_decode_equals_link_of_the_grown_request():
     _, o2, _, _, _ = oracle.decode_attention(lens, suffix + 2, k, ck, cv, kk[:n_s + 2], vv[:n_s + 2],
                                              q[n_s + 2:], kk[n_s + 2:], vv[n_s + 2:])
     assert np.allclose(np.concatenate([o1, o2]), out, rtol=0, atol=1e-12)
+
+
+def test_dummy_compile_matches_hf_llama():
+    """LegoLink-0's compile (Sec. 5.4): the dummy tokens and the chunk are one
+    ordinary Llama prefill at positions 0..n_dummy+L-1 whose first n_dummy rows
+    are dropped; hidden states and K/V of the chunk rows match the HuggingFace
+    forward of the whole sequence."""
+    ws, fn = _tiny_weights(2)
+    nd, L = 4, 21
+    rng = np.random.default_rng(13)
+    bos = rng.standard_normal(TINY["hidden"])
+    dummy = np.tile(bos, (nd, 1))
+    emb = rng.standard_normal((L, TINY["hidden"]))
+    out, kv = oracle.compile_chunk(emb, ws, fn, bf16_storage=False, dummy_emb=dummy, **TINY)
+    assert out.shape[0] == L and all(k.shape[0] == L and v.shape[0] == L for k, v in kv)
+    m = _hf_model(ws, fn)
+    seq = np.concatenate([dummy, emb])
+    with torch.no_grad():
+        r = m(inputs_embeds=torch.from_numpy(seq)[None], position_ids=torch.arange(nd + L)[None], use_cache=True)
+    np.testing.assert_allclose(out, r.last_hidden_state[0].numpy()[nd:], atol=2e-5, rtol=0)
+    for layer, (k, v) in enumerate(kv):
+        hk = r.past_key_values.layers[layer].keys[0].permute(1, 0, 2).numpy()[nd:]
+        hv = r.past_key_values.layers[layer].values[0].permute(1, 0, 2).numpy()[nd:]
+        np.testing.assert_allclose(k, hk, atol=2e-5, rtol=0)
+        np.testing.assert_allclose(v, hv, atol=2e-5, rtol=0)
+
+
+def test_dummy_compile_equals_link_after_cached_dummies():
+    """The dummies form an exact prefix: compiling them alone as chunk 0 and linking
+    the chunk as a suffix (k = 0, so nothing of chunk 0 is recomputed) gives the
+    dummy compile's K/V and hidden states; and the dummies change the cache (the
+    result differs from the plain compile)."""
+    ws, fn = _tiny_weights(2)
+    nd, L = 4, 13
+    rng = np.random.default_rng(17)
+    dummy = np.tile(rng.standard_normal(TINY["hidden"]), (nd, 1))
+    emb = rng.standard_normal((L, TINY["hidden"]))
+    out, kv = oracle.compile_chunk(emb, ws, fn, bf16_storage=False, dummy_emb=dummy, **TINY)
+    caches = _compile_all(ws, fn, [nd], dummy, bf16=False)
+    s, out_l, kv_l = oracle.link_model(emb, [nd], L, 0, ws, fn, caches, bf16_storage=False, **TINY)
+    assert s.tolist() == list(range(nd, nd + L))
+    np.testing.assert_allclose(out, out_l, atol=1e-10, rtol=0)
+    for (k1, v1), (k2, v2) in zip(kv, kv_l):
+        np.testing.assert_allclose(k1, k2, atol=1e-10, rtol=0)
+        np.testing.assert_allclose(v1, v2, atol=1e-10, rtol=0)
+    _, kv0 = oracle.compile_chunk(emb, ws, fn, bf16_storage=False, **TINY)
+    assert np.abs(kv0[0][0] - kv[0][0]).max() > 1e-3

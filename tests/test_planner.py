@@ -299,3 +299,84 @@ def test_decode_after_a_suffix_free_link_starts_a_block():
     with pytest.raises(el.EpicError) as e:                           # negative count
         el.epic_plan_decode(sizes, buf, [-1], cfg, [5], 8)
     assert e.value.status == 1
+
+
+def _compile_chunks(rng, n, max_len=90):
+    lens = [int(x) for x in rng.integers(1, max_len, size=n)]
+    blocks, nxt = [], 0
+    for L in lens:
+        nb = -(-L // 16)
+        blocks.append(list(range(nxt, nxt + nb)))
+        nxt += nb
+    return lens, blocks, nxt
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_plain_compile_plan_is_the_link_plan_of_suffix_only_requests(seed):
+    """Without dummies the compile plan is the link plan of one request per chunk with
+    no cached chunks, the chunk's tokens as suffix and the chunk blocks as free list."""
+    rng = np.random.default_rng(300 + seed)
+    lens, blocks, n = _compile_chunks(rng, int(rng.integers(1, 6)))
+    cfg = el.attn_cfg(8, 2, 64)
+    cs, cbuf, cv = el.epic_plan_compile(lens, blocks, 0, cfg, [], n)
+    ls, lbuf, lv = el.epic_plan_link([el.Request([], [], L, 0) for L in lens], cfg,
+                                     [b for bl in blocks for b in bl], n)
+    for f in ("batch", "n_s", "n_linked_blocks", "n_private", "n_tiles", "n_work", "n_partials", "max_pos",
+              "total_ints"):
+        assert getattr(cs, f) == getattr(ls, f), f
+    assert np.array_equal(cbuf, lbuf)
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("nd", [1, 4, 16, 21])
+def test_dummy_compile_plan(seed, nd):
+    """LegoLink-0 compile plan: chunk j's S rows are nd dummies then its L tokens at
+    positions 0..nd+L-1, linked through staging blocks taken from the free list in
+    order; each chunk block is written once more, outside the linked table, with
+    chunk token t (row s_off[j] + nd + t) at slot t and zeros past the chunk's end."""
+    rng = np.random.default_rng(400 + seed)
+    lens, blocks, n = _compile_chunks(rng, int(rng.integers(1, 6)))
+    cfg = el.attn_cfg(8, 2, 64)
+    need = sum(-(-(nd + L) // 16) for L in lens)
+    free = list(range(n, n + need + 5))
+    sizes, _, v = el.epic_plan_compile(lens, blocks, nd, cfg, free, n + need + 5)
+    _check_linked(v, len(lens))
+    assert sizes.n_s == sum(nd + L for L in lens) and sizes.max_pos == nd + max(lens)
+    assert v["linked_blocks"].tolist() == free[:need]
+    rows = v["priv_rows"].reshape(-1, 16)
+    pv = {int(b): i for i, b in enumerate(v["priv_block"])}
+    assert len(pv) == sizes.n_private == need + sum(len(b) for b in blocks)
+    assert np.all(v["priv_src"] == -1)
+    for j, (L, bl) in enumerate(zip(lens, blocks)):
+        a, b = v["s_off"][j], v["s_off"][j + 1]
+        assert v["s_pos"][a:b].tolist() == list(range(nd + L)) and np.all(v["s_req"][a:b] == j)
+        for i, bid in enumerate(bl):
+            want = [a + nd + i * 16 + o if i * 16 + o < L else -1 for o in range(16)]
+            assert rows[pv[bid]].tolist() == want
+        assert not set(bl) & set(v["linked_blocks"].tolist())
+    # every S row is stored once in the linked layout; chunk rows once more in their chunk block
+    counts = np.bincount(rows[rows >= 0], minlength=sizes.n_s)
+    for j, L in enumerate(lens):
+        a = v["s_off"][j]
+        assert np.all(counts[a:a + nd] == 1) and np.all(counts[a + nd:a + nd + L] == 2)
+
+
+def test_compile_plan_errors():
+    cfg = el.attn_cfg(8, 8, 64)
+    with pytest.raises(el.EpicError) as e:                   # too few staging blocks
+        el.epic_plan_compile([30], [[0, 1]], 4, cfg, [2, 3], 8)
+    assert e.value.status == 3
+    with pytest.raises(el.EpicError) as e:                   # staging block is a chunk block
+        el.epic_plan_compile([30], [[0, 1]], 4, cfg, [1, 2, 3], 8)
+    assert e.value.status == 1
+    with pytest.raises(el.EpicError) as e:                   # a block listed for two chunks
+        el.epic_plan_compile([10, 10], [[0], [0]], 0, cfg, [], 8)
+    assert e.value.status == 1
+    with pytest.raises(el.EpicError) as e:                   # wrong number of blocks
+        el.epic_plan_compile([30], [[0]], 0, cfg, [], 8)
+    assert e.value.status == 1
+    with pytest.raises(el.EpicError) as e:                   # negative dummy count
+        el.epic_plan_compile([30], [[0, 1]], -1, cfg, [], 8)
+    assert e.value.status == 1
+    s, _, v = el.epic_plan_compile([], [], 4, cfg, [], 8)    # nothing to compile
+    assert s.n_s == 0 and s.n_private == 0
