@@ -45,6 +45,8 @@ WORKLOADS = {
     # link step (k = 0) over those caches
     "c3compile": ("c3", {}),
     "c3lego0": ("c3", {"k": 0}),
+    # TTFT against context length at 512-token chunks: recompute-all (FR) vs LegoLink-16
+    "sweep512": ("c3", {"chunk_len": 512, "k": 16}),
     # decode after the link step (one new token per request), not the default line
     "c5k32dec": ("c5", {"k": 32}),
     "c4dec": ("c4", {}),
@@ -255,6 +257,64 @@ def bench_compile(args, wl, n_dummy: int):
     print(json.dumps(result), flush=True)
 
 
+def bench_sweep(args, wl, contexts=(2048, 4096, 8192, 16384, 32768, 65536)):
+    """TTFT against context length with 512-token chunks and a 128-token suffix, on
+    the 32-layer Llama-3-8B shape: FR prefills all N + 128 tokens (no chunk caches are
+    compiled, as for FR in the paper's long-context experiment), LegoLink-16 links
+    caches compiled beforehand by the library (untimed) and recomputes 16 tokens of
+    every chunk but the first plus the suffix.  Weights are drawn once, reused."""
+    import dataclasses
+
+    import numpy as np
+    import torch
+
+    from paper_2410_15332_amd import harness
+
+    weights = None
+    points = []
+    for n_ctx in contexts:
+        m = n_ctx // wl.chunk_lens[0]
+        row = {"context_tokens": n_ctx, "chunks": m}
+        for method, k in (("legolink16", 16), ("fr", -1)):
+            w2 = dataclasses.replace(wl, name=f"sweep_{method}_{n_ctx}", chunk_lens=[wl.chunk_lens[0]] * m, k=k)
+            t0 = time.time()
+            st = harness.stage_model(w2, caches="compile" if k >= 0 else "none", weights_on_device=True,
+                                     weights=weights)
+            weights = st.weights
+            st.run()
+            torch.cuda.synchronize()
+            reps = max(1, min(args.steps, 10 if k >= 0 else 3))
+            times = []
+            for _ in range(reps):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                st.run()
+                b.record()
+                torch.cuda.synchronize()
+                times.append(a.elapsed_time(b))
+            ms = float(np.median(times))
+            row[f"{method}_ms"] = round(ms, 3)
+            row[f"{method}_rows"] = st.sizes.n_s
+            log(f"N={n_ctx} {method}: {st.sizes.n_s} rows, TTFT {ms:.3f} ms (median of {reps}; staged in "
+                f"{time.time() - t0:.1f}s)")
+            del st
+            torch.cuda.empty_cache()
+        row["speedup"] = round(row["fr_ms"] / row["legolink16_ms"], 2)
+        points.append(row)
+    last = points[-1]
+    result = {
+        "metric": "TTFT (ms) against context length, 512-token chunks: FR vs LegoLink-16",
+        "value": last["legolink16_ms"], "unit": "ms (LegoLink-16 TTFT at the longest context)", "n_gpus": 1,
+        "steps": args.steps, "warmup": 1, "ms_per_step": last["legolink16_ms"], "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (random-init weights, seeded N(0,1) token embeddings)",
+        "config": {"workload": f"long-context sweep, {wl.n_layers}-layer Llama-3-8B shape, 512-token chunks, "
+                               f"{wl.suffix_len}-token suffix", "parallelism": "single GPU"},
+        "points": points,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def bench_model(args, wl, n_dummy: int = 0):
     """Full-model link step (all decoder layers + final norm) on the 32-layer configuration."""
     import numpy as np
@@ -398,6 +458,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     name, kw = WORKLOADS[args.workload]
     wl = get_config(name, **kw)
+    if args.workload == "sweep512":
+        bench_sweep(args, wl)
+        return
     if args.workload == "c3compile":
         bench_compile(args, wl, 4)
         return

@@ -306,13 +306,15 @@ def stage_compile(wl, cfg, layers, final_norm, chunk_blocks, free, num_blocks, n
 
 def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: float = 0.5, device="cuda",
                 threads: int = 8, weights_on_device: bool = False, n_dummy: int = 0,
-                keep_compile: bool = False) -> ModelStage:
+                keep_compile: bool = False, weights: List[Dict[str, object]] = None) -> ModelStage:
     """Weights, per-chunk caches, link plan and S-row embeddings for a model-level workload.
 
     caches="compile": every chunk is compiled on the GPU by the library itself
     (epic_plan_compile + epic_link_model, positions 0..L-1; with n_dummy > 0,
     LegoLink-0's compile: n_dummy copies of one dummy token first, dropped after);
-    caches="synthetic": every layer's chunk caches are seeded N(0, cache_scale^2) draws.
+    caches="synthetic": every layer's chunk caches are seeded N(0, cache_scale^2) draws;
+    caches="none": the pool stays zero (for k < 0, where no cached row is read).
+    weights: per-layer device tensors from an earlier stage of the same shape, reused.
     weights_on_device: draw the weights with a seeded device generator (timing runs)
     instead of synth.model_weights (parity runs).
     """
@@ -322,9 +324,11 @@ def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: 
     cfg = model_cfg(wl, L)
     hq, hkv, d, H = wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.hidden
     acfg = cfg.attn
-    weights, layers = [], []
+    given, weights, layers = weights, [], []
     for layer in range(L):
-        if weights_on_device:
+        if given is not None:
+            tw = given[layer]
+        elif weights_on_device:
             tw = _device_weights(wl, layer, device)
         else:
             w = synth.model_weights(wl.seed, layer, H, wl.ffn, hq, hkv, d, threads=threads)
