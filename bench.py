@@ -37,6 +37,8 @@ WORKLOADS = {
     "c5k4": ("c5", {"k": 4}),
     "c5k0": ("c5", {"k": 0}),
     "c5all": ("c5", {"k": -1}),
+    # the same long-context link step with cached K re-rotated to its linked positions
+    "c5k32rr": ("c5", {"k": 32}),
     "c4": ("c4", {}),
     "c2": ("c2", {}),
     "c1": ("c1", {}),
@@ -471,10 +473,12 @@ def main():
         bench_decode(args, wl)
         return
     t0 = time.time()
-    st = harness.stage_attention(wl, device="cuda", split_blocks=args.split_blocks)
+    rr_theta = 500000.0 if args.workload.endswith("rr") else 0.0
+    st = harness.stage_attention(wl, device="cuda", split_blocks=args.split_blocks, rerotate_theta=rr_theta)
     torch.cuda.synchronize()
     log(f"staged {wl.name}: n_s={st.sizes.n_s} tiles={st.sizes.n_tiles} work={st.sizes.n_work} "
-        f"partials={st.sizes.n_partials} in {time.time() - t0:.1f}s")
+        f"partials={st.sizes.n_partials} private={st.sizes.n_private} re-rotated={st.sizes.n_rerotated} "
+        f"in {time.time() - t0:.1f}s")
     flops = harness.attention_flops(st.views, wl.num_q_heads, wl.head_dim)
 
     if args.calibrate_copy_mib > 0:
@@ -541,6 +545,7 @@ def main():
             "block_size": 16,
             "recomputed_rows": n_s,
             "linked_tokens": int(st.sizes.max_pos),
+            "rerotate_cached_k": bool(rr_theta),
             "parallelism": "single GPU",
         },
         "ttft_ms": round(step_ms, 5),

@@ -64,7 +64,9 @@ const char* epic_version(void);
  * kv_split_blocks: key blocks per split-KV work item (0 = library default);
  * rows whose keys span several work items are merged with a log-sum-exp combine.
  * tile_rows: query rows (S row x head) per attention workgroup, 128 or 256
- * (0 = library default: 256 when the rows of a tile need nearly the same keys). */
+ * (0 = library default: 256 when the rows of a tile need nearly the same keys).
+ * rope_theta: the rotary base theta (inverse frequency theta^(-2i/D), pairs (i, i + D/2))
+ * that cached K was rotated with; a plan with re-rotated blocks needs it > 0. */
 typedef struct {
   int32_t num_q_heads;
   int32_t num_kv_heads;
@@ -73,13 +75,21 @@ typedef struct {
   float softmax_scale;
   int32_t kv_split_blocks;
   int32_t tile_rows;
+  float rope_theta;    /* rotary base of the cached K; used only by plans that re-rotate (else may be 0) */
 } epic_attn_cfg;
 
 /* One request, host memory, caller-owned.
  * chunk_blocks[chunk_block_off[j] .. chunk_block_off[j+1]) are the physical
  * blocks of chunk j in token order: token t of the chunk is in block t / bs at
  * offset t % bs; a chunk needs exactly ceil(chunk_len[j] / bs) blocks.
- * Chunk ids may repeat inside a request and across requests (shared caches). */
+ * Chunk ids may repeat inside a request and across requests (shared caches).
+ * Cached K is stored rotated at the chunk's own positions 0..L-1 (the compile
+ * step).  By default the link reuses it as stored (the paper reuses cached KV
+ * unchanged).  rerotate = 1 instead rotates the cached K rows of every chunk j > 0
+ * by its linked offset off_j (RoPE composes, so R(off_j) R(t) = R(off_j + t)): all
+ * blocks of those chunks become private copies, written by the link write with K
+ * rotated in fp32 from float64 angles and rounded to bf16, V copied unchanged.
+ * Chunk 0 (offset 0) stays shared.  Ignored for k < 0 (every token recomputed). */
 typedef struct {
   int32_t num_chunks;
   const int32_t* chunk_len;        /* [num_chunks], each >= 1 */
@@ -87,6 +97,7 @@ typedef struct {
   const int32_t* chunk_blocks;     /* physical block ids */
   int32_t suffix_len;              /* mutable tokens after the chunks, >= 0 */
   int32_t k;                       /* LegoLink-k; k < 0 = recompute every token */
+  int32_t rerotate;                /* 1: cached K of chunk j > 0 is re-rotated to its linked positions */
 } epic_link_request;
 
 /* Sizes of a plan for a batch of requests. */
@@ -100,6 +111,7 @@ typedef struct {
   int32_t n_partials;       /* split-KV partial results (per KV head) */
   int32_t tile_rows;        /* query rows (S row x head) per tile: 128 or 256 */
   int32_t max_pos;          /* 1 + largest linked position in the batch */
+  int32_t n_rerotated;      /* private blocks whose copied rows are re-rotated */
   int64_t total_ints;       /* int32 entries of the plan buffer */
 } epic_plan_sizes;
 
@@ -117,6 +129,8 @@ typedef struct {
  *   priv_block[n_private] private block ids (taken from free_blocks in order)
  *   priv_src[n_private]   shared block copied into it first, or -1
  *   priv_rows[n_private * block_size]  S row stored in each slot, or -1
+ *   priv_rot[n_private]   linked offset by which the rows copied from priv_src are
+ *                         re-rotated (K only), or 0
  *   tiles[n_tiles * 4]    (first S row, S rows, first partial or -1, splits)
  *   work[n_work * 8]      (tile, first linked block, end linked block, partial or -1,
  *                         leading 4-block KV tiles that need no mask, 0, 0, 0)
@@ -135,6 +149,7 @@ typedef struct {
   int32_t* priv_rows;
   int32_t* tiles;
   int32_t* work;
+  int32_t* priv_rot;
 } epic_plan;
 
 /* Host only, integer, synchronous.  Validates the requests and computes the
@@ -215,8 +230,9 @@ epic_status epic_plan_compile(const epic_compile_batch* batch, const epic_attn_c
 size_t epic_link_workspace_bytes(const epic_attn_cfg* cfg, const epic_plan_sizes* sizes);
 
 /* One attention layer of the link step (Sec. 4.2, Eq. 1), on the device:
- *   1. build every private block: copy its source block (if any), then store
- *      k_s / v_s of the S rows into their slots (bit-exact copies);
+ *   1. build every private block: copy its source block (if any; K rotated by
+ *      priv_rot when that is non-zero, see epic_link_request.rerotate), then
+ *      store k_s / v_s of the S rows into their slots (bit-exact copies);
  *   2. for each S row r at linked position p and query head h: softmax over the
  *      linked keys at positions <= p of scale * <q, k>, times V; write out[r, h]
  *      (bf16) and lse[r, h] = natural log of the softmax denominator (fp32).

@@ -10,8 +10,9 @@ no blocking or fusion beyond processing independent query rows in groups.
 
 Contents
   link.py   -- token selection (Sec. 4.2), KV expansion (Sec. 4.2, third step),
-               masked attention (Eq. 1), attention-level link step, and decode
-               after it (new tokens over the linked sequence).
+               masked attention (Eq. 1), attention-level link step, decode
+               after it (new tokens over the linked sequence), the rotary
+               embedding and the cached-K re-rotation variant.
   model.py  -- Llama-style decoder layer for the selected rows, the compile step
                (Sec. 2.2), the full-model link step, and the layer's row-set
                projections on their own.
@@ -29,6 +30,7 @@ from .link import (  # noqa: F401
     masked_attention,
     link_attention,
     decode_attention,
+    rerotate_cached,
 )
 from .model import (  # noqa: F401
     projection,

@@ -10,7 +10,9 @@ Readings where the paper is silent (each one is a choice):
     recompute-everything to equal an ordinary prefill);
   * MASK is additive -inf (a masked key gets zero weight), and a token attends
     to itself (key position <= query position);
-  * cached K keeps the rotary phase it was compiled with (no re-rotation);
+  * cached K keeps the rotary phase it was compiled with (no re-rotation); the
+    re-rotation variant (``rerotate_theta``) instead rotates chunk j's cached K
+    by its linked offset, stored again as bf16;
   * k larger than a chunk recomputes the whole chunk; k = 0 recomputes only the
     suffix (the Naive scheme of Sec. 2.3); k < 0 means recompute every token
     including the first chunk (FR, Sec. 2.3);
@@ -21,6 +23,41 @@ from __future__ import annotations
 from typing import List, Sequence, Tuple
 
 import numpy as np
+
+
+def _round_bf16(x: np.ndarray) -> np.ndarray:
+    """float64 -> float32 -> bf16 (nearest, ties to even) -> float64."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    u = (u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) & np.uint32(0xFFFF0000)
+    return u.view(np.float32).astype(np.float64)
+
+
+def rope(x: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
+    """Rotate [n, H, d] by linked positions pos [n]; pairs (i, i + d/2), angle pos * theta^(-2i/d)."""
+    d = x.shape[-1]
+    half = d // 2
+    inv_freq = theta ** (-np.arange(half, dtype=np.float64) * 2.0 / d)
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]      # [n, d/2]
+    cos = np.cos(ang)[:, None, :]
+    sin = np.sin(ang)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
+
+
+def rerotate_cached(cached_k: Sequence[np.ndarray], chunk_lens: Sequence[int], theta: float,
+                    bf16_storage: bool = True) -> List[np.ndarray]:
+    """Re-rotation variant of the cached K: chunk j's rows were rotated at their own
+    positions t, so rotating them by the chunk's linked offset off_j puts them at
+    off_j + t (rotations compose).  Chunk 0 (offset 0) is unchanged.  With
+    bf16_storage the rotated rows are rounded to bf16, as a stored cache is."""
+    out = []
+    for j, (ck, off) in enumerate(zip(cached_k, chunk_offsets(chunk_lens))):
+        if j == 0 or off == 0:
+            out.append(ck)
+            continue
+        r = rope(np.asarray(ck, np.float64), np.full(ck.shape[0], off), theta)
+        out.append(_round_bf16(r) if bf16_storage else r)
+    return out
 
 
 def chunk_offsets(chunk_lens: Sequence[int]) -> List[int]:
@@ -116,12 +153,17 @@ def masked_attention(q: np.ndarray, K_exp: np.ndarray, V_exp: np.ndarray, s_pos:
 def link_attention(chunk_lens: Sequence[int], suffix_len: int, k: int,
                    cached_k: Sequence[np.ndarray], cached_v: Sequence[np.ndarray],
                    q_s: np.ndarray, k_s: np.ndarray, v_s: np.ndarray,
-                   scale: float | None = None, rows: Sequence[int] | None = None):
+                   scale: float | None = None, rows: Sequence[int] | None = None,
+                   rerotate_theta: float | None = None):
     """One attention layer of the link step for one request.
 
     q_s, k_s, v_s are the recomputed rows of S in ascending position order
-    (already projected and rotated).  Returns (s_pos, out, lse, K_exp, V_exp).
+    (already projected and rotated).  rerotate_theta: the re-rotation variant
+    (cached K moved to its linked positions, rotary base theta; not for k < 0).
+    Returns (s_pos, out, lse, K_exp, V_exp).
     """
+    if rerotate_theta is not None and k >= 0:
+        cached_k = rerotate_cached(cached_k, chunk_lens, rerotate_theta)
     s_pos = legolink_positions(chunk_lens, suffix_len, k)
     if len(s_pos) != q_s.shape[0]:
         raise ValueError(f"|S| = {len(s_pos)} but {q_s.shape[0]} query rows were given")

@@ -26,7 +26,7 @@ from typing import Dict, List, Sequence, Tuple
 
 import numpy as np
 
-from .link import expand_kv, legolink_positions, masked_attention
+from .link import _round_bf16, expand_kv, legolink_positions, masked_attention, rerotate_cached, rope  # noqa: F401
 
 
 def _bf16_to_f64(bits: np.ndarray) -> np.ndarray:
@@ -34,28 +34,9 @@ def _bf16_to_f64(bits: np.ndarray) -> np.ndarray:
     return u.view(np.float32).astype(np.float64)
 
 
-def _round_bf16(x: np.ndarray) -> np.ndarray:
-    """float64 -> float32 -> bf16 (nearest, ties to even) -> float64."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    u = (u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) & np.uint32(0xFFFF0000)
-    return u.view(np.float32).astype(np.float64)
-
-
 def rmsnorm(x: np.ndarray, w: np.ndarray, eps: float) -> np.ndarray:
     """x / sqrt(mean(x^2) + eps) * w, row-wise."""
     return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * w
-
-
-def rope(x: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
-    """Rotate [n, H, d] by linked positions pos [n]; pairs (i, i + d/2), angle pos * theta^(-2i/d)."""
-    d = x.shape[-1]
-    half = d // 2
-    inv_freq = theta ** (-np.arange(half, dtype=np.float64) * 2.0 / d)
-    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]      # [n, d/2]
-    cos = np.cos(ang)[:, None, :]
-    sin = np.sin(ang)[:, None, :]
-    x1, x2 = x[..., :half], x[..., half:]
-    return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
 
 
 def _silu(x: np.ndarray) -> np.ndarray:
@@ -115,12 +96,14 @@ def link_model(emb_s: np.ndarray, chunk_lens: Sequence[int], suffix_len: int, k:
                weights: Sequence[Dict[str, np.ndarray]], final_norm: np.ndarray,
                caches: Sequence[Tuple[Sequence[np.ndarray], Sequence[np.ndarray]]],
                hidden: int, ffn: int, hq: int, hkv: int, d: int, theta: float, eps: float,
-               bf16_storage: bool = True):
+               bf16_storage: bool = True, rerotate: bool = False):
     """Full-model link step for one request.
 
     emb_s [nS, hidden]: layer-0 hidden rows of S (embeddings of those tokens),
     in ascending position order.  caches[l] = (chunk K list, chunk V list) of
     layer l, each [L_j, Hkv, d] as compiled (float64 values of bf16 data).
+    rerotate: cached K of chunks j > 0 is first moved to its linked positions
+    (re-rotation variant, see link.rerotate_cached; not for k < 0).
     Returns (s_pos, out [nS, hidden] after the final norm, per-layer recomputed
     (k, v) of S).
     """
@@ -133,6 +116,8 @@ def link_model(emb_s: np.ndarray, chunk_lens: Sequence[int], suffix_len: int, k:
     new_kv = []
     for layer, w in enumerate(weights):
         ck, cv = caches[layer] if caches else ([], [])
+        if rerotate and k >= 0:
+            ck = rerotate_cached(ck, chunk_lens, theta, bf16_storage)
         h, ks, vs = _layer(h, s_pos, w, cfg, ck, cv, n_total, bf16_storage)
         new_kv.append((ks, vs))
     out = rmsnorm(h, _bf16_to_f64(final_norm), eps)

@@ -6,6 +6,7 @@
 #include <cstdint>
 
 #include "kernels.h"
+#include "link_write.h"
 #include "plan_internal.h"
 #include "status.h"
 
@@ -33,6 +34,8 @@ epic_status check_plan(const epic_plan_sizes* s, const epic_plan* p) {
     EPIC_CHECK_ARG(p->s_pos && p->linked_blocks && p->block_pos0 && p->block_len && p->tiles && p->work,
                    "device plan arrays are NULL");
   if (s->n_private > 0) EPIC_CHECK_ARG(p->priv_block && p->priv_src && p->priv_rows, "private block arrays are NULL");
+  EPIC_CHECK_ARG(s->n_rerotated >= 0 && s->n_rerotated <= s->n_private, "bad plan sizes (re-rotated blocks)");
+  if (s->n_rerotated > 0) EPIC_CHECK_ARG(p->priv_rot != nullptr, "priv_rot is NULL");
   return EPIC_OK;
 }
 
@@ -71,7 +74,12 @@ epic_status run_link_attention(const epic_attn_cfg* cfg, const epic_plan_sizes* 
                                void* workspace, void* stream_ptr) {
   hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
   record_event(0, stream);
-  launch_link_write(p, s->n_private, cfg->num_kv_heads, cfg->head_dim, k_s, v_s, k_cache, v_cache, stream);
+  if (s->n_rerotated > 0)
+    launch_link_write_rotated(p, s->n_private, cfg->num_kv_heads, cfg->head_dim, cfg->rope_theta, k_s, v_s, k_cache,
+                              v_cache, stream);
+  else
+    launch_link_write(p, s->n_private, cfg->num_kv_heads, cfg->head_dim, k_s, v_s, k_cache, v_cache, stream);
+  if (s->n_s == 0) return hip_status("link write launch");   // re-rotated copies only
   AttnArgs a{};
   a.s_pos = p->s_pos;
   a.linked_blocks = p->linked_blocks;
@@ -115,7 +123,13 @@ extern "C" epic_status epic_link_attention(const epic_attn_cfg* cfg, const epic_
   if (st != EPIC_OK) return st;
   st = check_plan(sizes, plan_dev);
   if (st != EPIC_OK) return st;
-  if (sizes->n_s == 0) return EPIC_OK;
+  if (sizes->n_rerotated > 0 && !(cfg->rope_theta > 1.0f))
+    return fail(EPIC_ERR_INVALID_ARG, "plan re-rotates cached K: rope_theta %g must be > 1", cfg->rope_theta);
+  if (sizes->n_s == 0 && sizes->n_private == 0) return EPIC_OK;
+  EPIC_CHECK_ARG(k_cache && v_cache && aligned16(k_cache) && aligned16(v_cache), "KV caches NULL or unaligned");
+  if (sizes->n_s == 0)
+    return run_link_attention(cfg, sizes, plan_dev, nullptr, nullptr, nullptr, k_cache, v_cache, nullptr, nullptr,
+                              nullptr, stream);
   EPIC_CHECK_ARG(q_s && k_s && v_s && k_cache && v_cache && out, "NULL tensor argument");
   EPIC_CHECK_ARG(aligned16(q_s) && aligned16(k_s) && aligned16(v_s) && aligned16(k_cache) && aligned16(v_cache) &&
                      aligned16(out),

@@ -15,6 +15,7 @@
 #include <cstdint>
 
 #include "gemm.h"
+#include "link_write.h"
 #include "kernels.h"
 #include "plan_internal.h"
 #include "status.h"
@@ -115,7 +116,9 @@ epic_status run_layer(const epic_model_cfg* c, const epic_layer_weights* w, cons
   g.tile_count = ws.gemm_count;
   launch_gemm(g, kStoreF32, stream);
   launch_rope_split(ws.qkv, ws.cs, ws.q, ws.k, ws.v, n, hq, hkv, D, stream);
-  epic_status st = run_link_attention(&c->attn, s, p, ws.q, ws.k, ws.v, kc, vc, ws.o, nullptr, ws.attn, stream);
+  epic_attn_cfg ac = c->attn;
+  ac.rope_theta = c->rope_theta;            // cached K was rotated with the model's base
+  epic_status st = run_link_attention(&ac, s, p, ws.q, ws.k, ws.v, kc, vc, ws.o, nullptr, ws.attn, stream);
   if (st != EPIC_OK) return st;
   g = GemmArgs{};
   g.A = ws.o;
@@ -158,6 +161,9 @@ epic_status check_common(const epic_model_cfg* c, const epic_plan_sizes* s, cons
   if (st != EPIC_OK) return st;
   EPIC_CHECK_ARG(s && p, "plan is NULL");
   EPIC_CHECK_ARG(valid_tile_rows(s->tile_rows), "plan tile rows %d unsupported", s->tile_rows);
+  EPIC_CHECK_ARG(s->n_rerotated >= 0 && s->n_rerotated <= s->n_private, "bad plan sizes (re-rotated blocks)");
+  if (s->n_private > 0) EPIC_CHECK_ARG(p->priv_block && p->priv_src && p->priv_rows, "private block arrays are NULL");
+  if (s->n_rerotated > 0) EPIC_CHECK_ARG(p->priv_rot != nullptr, "priv_rot is NULL");
   if (s->n_s == 0) return EPIC_OK;
   EPIC_CHECK_ARG(p->s_pos && p->tiles && p->work && p->linked_blocks, "device plan arrays are NULL");
   EPIC_CHECK_ARG(h != nullptr && (reinterpret_cast<uintptr_t>(h) & 15u) == 0, "hidden_s must be 16-byte aligned");
@@ -190,7 +196,14 @@ extern "C" epic_status epic_link_layer(const epic_model_cfg* cfg, const epic_lay
                                        void* stream) {
   clear_error();
   epic_status st = check_common(cfg, sizes, plan_dev, hidden_s, workspace, workspace_bytes);
-  if (st != EPIC_OK || sizes->n_s == 0) return st;
+  if (st != EPIC_OK) return st;
+  if (sizes->n_s == 0) {                    // no rows: only the re-rotated copies, if any
+    if (sizes->n_rerotated == 0) return EPIC_OK;
+    EPIC_CHECK_ARG(k_cache && v_cache, "KV cache pointers are NULL");
+    launch_link_write_rotated(plan_dev, sizes->n_private, cfg->attn.num_kv_heads, cfg->attn.head_dim,
+                              cfg->rope_theta, nullptr, nullptr, k_cache, v_cache, static_cast<hipStream_t>(stream));
+    return hip_ok("link write launch");
+  }
   st = check_weights(w);
   if (st != EPIC_OK) return st;
   EPIC_CHECK_ARG(k_cache && v_cache, "KV cache pointers are NULL");
@@ -208,7 +221,18 @@ extern "C" epic_status epic_link_model(const epic_model_cfg* cfg, const epic_lay
                                        size_t workspace_bytes, void* stream) {
   clear_error();
   epic_status st = check_common(cfg, sizes, plan_dev, hidden_s, workspace, workspace_bytes);
-  if (st != EPIC_OK || sizes->n_s == 0) return st;
+  if (st != EPIC_OK) return st;
+  if (sizes->n_s == 0) {                    // no rows: only the re-rotated copies, if any
+    if (sizes->n_rerotated == 0) return EPIC_OK;
+    EPIC_CHECK_ARG(k_caches && v_caches, "KV cache pointers are NULL");
+    for (int l = 0; l < cfg->n_layers; ++l) {
+      EPIC_CHECK_ARG(k_caches[l] && v_caches[l], "layer %d: KV cache pointers are NULL", l);
+      launch_link_write_rotated(plan_dev, sizes->n_private, cfg->attn.num_kv_heads, cfg->attn.head_dim,
+                                cfg->rope_theta, nullptr, nullptr, k_caches[l], v_caches[l],
+                                static_cast<hipStream_t>(stream));
+    }
+    return hip_ok("link write launch");
+  }
   EPIC_CHECK_ARG(layers && k_caches && v_caches && final_norm && out_hidden, "NULL model argument");
   for (int l = 0; l < cfg->n_layers; ++l) {
     st = check_weights(&layers[l]);

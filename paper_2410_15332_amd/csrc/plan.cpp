@@ -44,8 +44,12 @@ int cdiv(int64_t a, int64_t b) { return static_cast<int>((a + b - 1) / b); }
 
 struct ReqShape {
   int64_t n_chunk_tokens = 0;
-  int n_s = 0, n_lb = 0, n_priv = 0;
+  int n_s = 0, n_lb = 0, n_priv = 0, n_rerot = 0;
 };
+
+// Re-rotation applies to the cached rows of chunks after the first (chunk 0 sits
+// at offset 0, where the compile rotation is already the linked one).
+bool rerotates(const epic_link_request& r, int j) { return r.rerotate != 0 && r.k >= 0 && j > 0; }
 
 // Number of tokens of chunk j that belong to S.
 int selected_in_chunk(const epic_link_request& r, int j) {
@@ -57,6 +61,7 @@ int selected_in_chunk(const epic_link_request& r, int j) {
 epic_status validate_request(const epic_link_request& r, int idx, ReqShape* sh) {
   EPIC_CHECK_ARG(r.num_chunks >= 0, "request %d: num_chunks %d < 0", idx, r.num_chunks);
   EPIC_CHECK_ARG(r.suffix_len >= 0, "request %d: suffix_len %d < 0", idx, r.suffix_len);
+  EPIC_CHECK_ARG(r.rerotate == 0 || r.rerotate == 1, "request %d: rerotate %d (0 or 1)", idx, r.rerotate);
   if (r.num_chunks > 0) {
     EPIC_CHECK_ARG(r.chunk_len && r.chunk_block_off && r.chunk_blocks,
                    "request %d: chunk arrays are NULL", idx);
@@ -73,7 +78,12 @@ epic_status validate_request(const epic_link_request& r, int idx, ReqShape* sh) 
     const int sel = selected_in_chunk(r, j);
     sh->n_s += sel;
     sh->n_lb += nb;
-    sh->n_priv += cdiv(sel, kBlock);
+    if (rerotates(r, j)) {
+      sh->n_priv += nb;                                   // every block: a rotated copy
+      sh->n_rerot += sel >= L ? 0 : nb - sel / kBlock;    // those that keep a cached row
+    } else {
+      sh->n_priv += cdiv(sel, kBlock);
+    }
   }
   sh->n_s += r.suffix_len;
   sh->n_lb += cdiv(r.suffix_len, kBlock);
@@ -287,7 +297,7 @@ void choose_tiles(const std::vector<ReqRows>& rr, const epic_attn_cfg* cfg, epic
 
 void finish_sizes(epic_plan_sizes* s) {
   s->total_ints = 3 * align16(s->n_s) + 2 * align16(s->batch + 1) + 3 * align16(s->n_linked_blocks) +
-                  2 * align16(s->n_private) + align16(int64_t(s->n_private) * kBlock) +
+                  3 * align16(s->n_private) + align16(int64_t(s->n_private) * kBlock) +
                   align16(4 * int64_t(s->n_tiles)) + align16(kWorkInts * int64_t(s->n_work));
 }
 
@@ -350,7 +360,7 @@ epic_status plan_shape(const epic_link_request* reqs, int32_t batch, const epic_
   if (st != EPIC_OK) return st;
   epic_plan_sizes s{};
   s.batch = batch;
-  int64_t n_s = 0, n_lb = 0, n_priv = 0, max_pos = 0;
+  int64_t n_s = 0, n_lb = 0, n_priv = 0, n_rerot = 0, max_pos = 0;
   for (int b = 0; b < batch; ++b) {
     ReqShape sh;
     st = validate_request(reqs[b], b, &sh);
@@ -358,6 +368,7 @@ epic_status plan_shape(const epic_link_request* reqs, int32_t batch, const epic_
     n_s += sh.n_s;
     n_lb += sh.n_lb;
     n_priv += sh.n_priv;
+    n_rerot += sh.n_rerot;
     max_pos = std::max<int64_t>(max_pos, sh.n_chunk_tokens + reqs[b].suffix_len);
   }
   EPIC_CHECK_ARG(n_s < (int64_t(1) << 30) && n_lb < (int64_t(1) << 30), "batch too large");
@@ -373,6 +384,7 @@ epic_status plan_shape(const epic_link_request* reqs, int32_t batch, const epic_
   s.n_s = static_cast<int32_t>(n_s);
   s.n_linked_blocks = static_cast<int32_t>(n_lb);
   s.n_private = static_cast<int32_t>(n_priv);
+  s.n_rerotated = static_cast<int32_t>(n_rerot);
   s.max_pos = static_cast<int32_t>(max_pos);
   finish_sizes(&s);
   *out = s;
@@ -412,6 +424,7 @@ extern "C" epic_status epic_plan_layout(const epic_plan_sizes* s, int32_t* base,
   p->priv_rows = take(int64_t(s->n_private) * kBlock);
   p->tiles = take(4 * int64_t(s->n_tiles));
   p->work = take(kWorkInts * int64_t(s->n_work));
+  p->priv_rot = take(s->n_private);
   if (cur - base != s->total_ints) return fail(EPIC_ERR_INVALID_ARG, "plan sizes are inconsistent");
   return EPIC_OK;
 }
@@ -466,11 +479,12 @@ extern "C" epic_status epic_plan_link(const epic_link_request* reqs, int32_t bat
         const int t0 = i * bs, len = std::min(bs, L - t0);
         plan->block_pos0[lb] = static_cast<int32_t>(off + t0);
         plan->block_len[lb] = len;
-        if (t0 < sel) {
+        if (t0 < sel || rerotates(r, j)) {
           const int id = free_blocks[pv];
           const bool keeps_cached = sel < t0 + len;  // some valid slot is not recomputed
           plan->priv_block[pv] = id;
           plan->priv_src[pv] = keeps_cached ? cb[i] : -1;
+          plan->priv_rot[pv] = keeps_cached && rerotates(r, j) ? static_cast<int32_t>(off) : 0;
           for (int o = 0; o < bs; ++o) {
             const int t = t0 + o;
             int32_t rr = -1;
@@ -500,6 +514,7 @@ extern "C" epic_status epic_plan_link(const epic_link_request* reqs, int32_t bat
       plan->linked_blocks[lb] = id;
       plan->priv_block[pv] = id;
       plan->priv_src[pv] = -1;
+      plan->priv_rot[pv] = 0;
       for (int o = 0; o < bs; ++o) {
         int32_t rr = -1;
         if (o < len) {
@@ -659,6 +674,7 @@ extern "C" epic_status epic_plan_decode(const epic_plan_sizes* prev_sizes, const
       const int id = prev->linked_blocks[d.e - 1], len = prev->block_len[d.e - 1];
       plan->priv_block[pv] = id;
       plan->priv_src[pv] = id;                 // its earlier tokens stay: copied onto themselves
+      plan->priv_rot[pv] = 0;
       for (int o = 0; o < bs; ++o)
         plan->priv_rows[int64_t(pv) * bs + o] = (o >= len && o < len + d.room) ? add_row(b, pos++, id, o) : -1;
       ++pv;
@@ -671,6 +687,7 @@ extern "C" epic_status epic_plan_decode(const epic_plan_sizes* prev_sizes, const
       plan->block_len[lb] = len;
       plan->priv_block[pv] = id;
       plan->priv_src[pv] = -1;
+      plan->priv_rot[pv] = 0;
       for (int o = 0; o < bs; ++o) plan->priv_rows[int64_t(pv) * bs + o] = o < len ? add_row(b, pos++, id, o) : -1;
     }
   }
@@ -798,6 +815,7 @@ extern "C" epic_status epic_plan_compile(const epic_compile_batch* batch, const 
       plan->block_len[lb] = len;
       plan->priv_block[pv] = id;
       plan->priv_src[pv] = -1;
+      plan->priv_rot[pv] = 0;
       for (int o = 0; o < bs; ++o) {
         int32_t r = -1;
         if (o < len) {
@@ -814,6 +832,7 @@ extern "C" epic_status epic_plan_compile(const epic_compile_batch* batch, const 
       for (int i = 0; i * bs < L; ++i, ++pv) {
         plan->priv_block[pv] = cbk[i];
         plan->priv_src[pv] = -1;
+        plan->priv_rot[pv] = 0;
         for (int o = 0; o < bs; ++o) {
           const int t = i * bs + o;
           plan->priv_rows[int64_t(pv) * bs + o] = t < L ? row0 + nd + t : -1;

@@ -48,12 +48,12 @@ _i32p = C.POINTER(C.c_int32)
 class epic_attn_cfg(C.Structure):
     _fields_ = [("num_q_heads", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32),
                 ("block_size", C.c_int32), ("softmax_scale", C.c_float), ("kv_split_blocks", C.c_int32),
-                ("tile_rows", C.c_int32)]
+                ("tile_rows", C.c_int32), ("rope_theta", C.c_float)]
 
 
 class epic_link_request(C.Structure):
     _fields_ = [("num_chunks", C.c_int32), ("chunk_len", _i32p), ("chunk_block_off", _i32p),
-                ("chunk_blocks", _i32p), ("suffix_len", C.c_int32), ("k", C.c_int32)]
+                ("chunk_blocks", _i32p), ("suffix_len", C.c_int32), ("k", C.c_int32), ("rerotate", C.c_int32)]
 
 
 class epic_compile_batch(C.Structure):
@@ -65,11 +65,11 @@ class epic_plan_sizes(C.Structure):
     _fields_ = [("batch", C.c_int32), ("n_s", C.c_int32), ("n_linked_blocks", C.c_int32),
                 ("n_private", C.c_int32), ("n_tiles", C.c_int32), ("n_work", C.c_int32),
                 ("n_partials", C.c_int32), ("tile_rows", C.c_int32), ("max_pos", C.c_int32),
-                ("total_ints", C.c_int64)]
+                ("n_rerotated", C.c_int32), ("total_ints", C.c_int64)]
 
 
 PLAN_FIELDS = ["s_pos", "s_req", "s_slot", "s_off", "linked_blocks", "block_pos0", "block_len", "blk_off",
-               "priv_block", "priv_src", "priv_rows", "tiles", "work"]
+               "priv_block", "priv_src", "priv_rows", "tiles", "work", "priv_rot"]
 
 
 class epic_plan(C.Structure):
@@ -165,10 +165,12 @@ class Request:
     chunk_blocks: List[List[int]]
     suffix_len: int
     k: int
+    rerotate: bool = False
 
 
-def attn_cfg(hq: int, hkv: int, d: int, scale: float = 0.0, split_blocks: int = 0, tile_rows: int = 0) -> epic_attn_cfg:
-    return epic_attn_cfg(hq, hkv, d, BLOCK, scale, split_blocks, tile_rows)
+def attn_cfg(hq: int, hkv: int, d: int, scale: float = 0.0, split_blocks: int = 0, tile_rows: int = 0,
+             rope_theta: float = 0.0) -> epic_attn_cfg:
+    return epic_attn_cfg(hq, hkv, d, BLOCK, scale, split_blocks, tile_rows, rope_theta)
 
 
 class _ReqArray:
@@ -185,7 +187,7 @@ class _ReqArray:
             self.keep += [lens, off, blocks]
             self.arr[i] = epic_link_request(len(r.chunk_lens), lens.ctypes.data_as(_i32p),
                                             off.ctypes.data_as(_i32p), blocks.ctypes.data_as(_i32p),
-                                            r.suffix_len, r.k)
+                                            r.suffix_len, r.k, int(r.rerotate))
         self.n = len(reqs)
 
 
@@ -267,7 +269,7 @@ def plan_views(sizes: epic_plan_sizes, buf: np.ndarray) -> dict:
             "linked_blocks": sizes.n_linked_blocks, "block_pos0": sizes.n_linked_blocks,
             "block_len": sizes.n_linked_blocks, "blk_off": sizes.batch + 1, "priv_block": sizes.n_private,
             "priv_src": sizes.n_private, "priv_rows": sizes.n_private * BLOCK, "tiles": 4 * sizes.n_tiles,
-            "work": WORK_INTS * sizes.n_work}
+            "work": WORK_INTS * sizes.n_work, "priv_rot": sizes.n_private}
     out = {}
     for name in PLAN_FIELDS:
         addr = C.cast(getattr(plan, name), C.c_void_p).value or base

@@ -109,20 +109,23 @@ def chunk_ids(wl: AttnWorkload) -> List[int]:
 
 
 def stage_attention(wl: AttnWorkload, device="cuda", split_blocks: int = 0, spare_blocks: int = 0,
-                    threads: int = 8, tile_rows: int = 0) -> AttnStage:
-    """Chunk pool + plan + S-row inputs + output buffers for an attention-level workload."""
+                    threads: int = 8, tile_rows: int = 0, rerotate_theta: float = 0.0) -> AttnStage:
+    """Chunk pool + plan + S-row inputs + output buffers for an attention-level workload.
+    rerotate_theta > 0: the re-rotation variant (cached K of chunks 1.. moved to its
+    linked positions, rotary base rerotate_theta)."""
     import torch
     from concurrent.futures import ThreadPoolExecutor
 
     hq, hkv, d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
-    cfg = el.attn_cfg(hq, hkv, d, 0.0, split_blocks, tile_rows)
+    cfg = el.attn_cfg(hq, hkv, d, 0.0, split_blocks, tile_rows, rerotate_theta)
+    rerotate = rerotate_theta > 0
     ids = chunk_ids(wl)
     nb = {c: -(-wl.chunk_lens[c] // el.BLOCK) for c in ids}
     n_chunk_blocks = sum(nb.values())
 
     def reqs_with(block_of):
-        return [el.Request([wl.chunk_lens[c] for c in r], [block_of[c] for c in r], wl.suffix_lens[i], wl.k)
-                for i, r in enumerate(wl.requests)]
+        return [el.Request([wl.chunk_lens[c] for c in r], [block_of[c] for c in r], wl.suffix_lens[i], wl.k,
+                           rerotate) for i, r in enumerate(wl.requests)]
 
     # private blocks needed: plan once with placeholder ids
     placeholder, nxt = {}, 0
@@ -306,7 +309,8 @@ def stage_compile(wl, cfg, layers, final_norm, chunk_blocks, free, num_blocks, n
 
 def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: float = 0.5, device="cuda",
                 threads: int = 8, weights_on_device: bool = False, n_dummy: int = 0,
-                keep_compile: bool = False, weights: List[Dict[str, object]] = None) -> ModelStage:
+                keep_compile: bool = False, weights: List[Dict[str, object]] = None,
+                rerotate: bool = False) -> ModelStage:
     """Weights, per-chunk caches, link plan and S-row embeddings for a model-level workload.
 
     caches="compile": every chunk is compiled on the GPU by the library itself
@@ -315,6 +319,7 @@ def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: 
     caches="synthetic": every layer's chunk caches are seeded N(0, cache_scale^2) draws;
     caches="none": the pool stays zero (for k < 0, where no cached row is read).
     weights: per-layer device tensors from an earlier stage of the same shape, reused.
+    rerotate: the link request re-rotates cached K to its linked positions.
     weights_on_device: draw the weights with a seeded device generator (timing runs)
     instead of synth.model_weights (parity runs).
     """
@@ -340,7 +345,7 @@ def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: 
 
     m = len(wl.chunk_lens)
     nb = [-(-x // el.BLOCK) for x in wl.chunk_lens]
-    link_req0 = el.Request(list(wl.chunk_lens), [[0] * n for n in nb], wl.suffix_len, wl.k)
+    link_req0 = el.Request(list(wl.chunk_lens), [[0] * n for n in nb], wl.suffix_len, wl.k, rerotate)
     n_priv = el.epic_plan_sizes_get([link_req0], acfg, 1 << 30).n_private
     # staging blocks of a dummy-token compile; free again once the compile is done
     n_stage = sum(-(-(n_dummy + x) // el.BLOCK) for x in wl.chunk_lens) if n_dummy > 0 else 0
@@ -372,7 +377,7 @@ def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: 
             k_caches[layer] = _bf16_tensor(kp, device)
             v_caches[layer] = _bf16_tensor(vp, device)
 
-    req = el.Request(list(wl.chunk_lens), chunk_blocks, wl.suffix_len, wl.k)
+    req = el.Request(list(wl.chunk_lens), chunk_blocks, wl.suffix_len, wl.k, rerotate)
     sizes, host, views = el.epic_plan_link([req], acfg, free, num_blocks)
     dplan = el.DevicePlan(sizes, host, device)
     emb = _tok_rows(wl, list(range(m)), wl.chunk_lens, wl.suffix_len, views["s_pos"])

@@ -52,9 +52,18 @@ def _sample_rows(n, seed, n_rand=48, tile=32):
     return np.array(sorted(rows), dtype=np.int64)
 
 
-def check_stage(st, sample=None, seed=0):
+def _ulp_bf16(x):
+    """Spacing of bf16 values at |x| (8 significant bits)."""
+    return np.exp2(np.floor(np.log2(np.maximum(np.abs(x), 1e-30))) - 7)
+
+
+def check_stage(st, sample=None, seed=0, rerotate_theta=None):
     """The 2e-2 output bar holds for N(0, 1) values; values drawn with a larger
-    scale c are weighted averages of vectors c times larger, so the bar scales by c."""
+    scale c are weighted averages of vectors c times larger, so the bar scales by c.
+    rerotate_theta: the re-rotation variant; its rotated cached K rows are fp32
+    rotations rounded to bf16 on the GPU and float64 ones on the oracle's side, so
+    they may differ by one bf16 step where the two round differently (or by the
+    fp32 error itself where a rotated value nearly cancels)."""
     el = _el()
     wl = st.wl
     torch.cuda.synchronize()
@@ -79,7 +88,7 @@ def check_stage(st, sample=None, seed=0):
                                                    wl.qk_scale))
         rows = None if sample is None else sample(len(s_ref), seed + r)
         _, o_ref, l_ref, K_exp, V_exp = oracle.link_attention(lens, wl.suffix_lens[r], wl.k, ck, cv, q, k, vv,
-                                                              rows=rows)
+                                                              rows=rows, rerotate_theta=rerotate_theta)
         idx = np.arange(len(s_ref)) if rows is None else rows
         got = out[a + idx]
         err = np.abs(got - o_ref).max() / max(1.0, wl.value_scale)
@@ -91,8 +100,25 @@ def check_stage(st, sample=None, seed=0):
         assert np.all(rel <= LSE_RTOL) or np.all(np.abs(gl - l_ref) <= LSE_RTOL), "lse off"
         # linked cache, read back through the linked block table: bit-exact
         gk, gv = el.read_linked_kv(kc, vc, v, r)
-        assert np.array_equal(_f64(gk), K_exp), f"request {r}: linked K differs"
         assert np.array_equal(_f64(gv), V_exp), f"request {r}: linked V differs"
+        if rerotate_theta is None or wl.k < 0:
+            assert np.array_equal(_f64(gk), K_exp), f"request {r}: linked K differs"
+        else:
+            rot = np.zeros(len(K_exp), bool)                 # cached rows of chunks 1..
+            offs = oracle.chunk_offsets(lens)
+            for j in range(1, len(lens)):
+                rot[offs[j]:offs[j] + lens[j]] = True
+            rot[s_ref] = False
+            gk64 = _f64(gk)
+            assert np.array_equal(gk64[~rot], K_exp[~rot]), f"request {r}: linked K differs (unrotated rows)"
+            diff = np.abs(gk64[rot] - K_exp[rot])
+            # one bf16 step of the larger value, plus the fp32 rotation's own error
+            # (cos / sin rounded to fp32: ~1e-7 of the pair's size), which matters where
+            # the rotated value nearly cancels and its bf16 step is tiny
+            tol = _ulp_bf16(np.maximum(np.abs(gk64[rot]), np.abs(K_exp[rot]))) + 1e-6 * max(1.0, wl.value_scale)
+            assert np.all(diff <= tol), f"request {r}: re-rotated K off by {(diff - tol).max()} beyond the bound"
+            print(f"[gpu-test] request {r}: re-rotated K elements one step off: {(diff > 0).mean():.2e}",
+                  flush=True)
     # shared chunk blocks are never written
     for c, ids in st.chunk_block_ids.items():
         kr, vr = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], hkv, d, wl.value_scale, qk_scale=wl.qk_scale)
@@ -221,3 +247,31 @@ def test_workspace_too_small_is_rejected():
         el.epic_link_attention(st.cfg, st.dplan, st.q_s, st.k_s, st.v_s, st.k_cache, st.v_cache, st.out,
                                st.lse, small)
     assert e.value.status == 4
+
+
+RR = [
+    _wl("rr_c1_like", [128] * 4, [[0, 1, 2, 3]], [16], 4, 8, 8, 64, 0.5),
+    _wl("rr_d128_ragged", [37, 100, 16, 51, 300], [[0, 1, 2, 3, 4]], [23], 16, 32, 8, 128),
+    _wl("rr_k0_batch", [70, 33, 129], [[0, 1, 2], [2, 0], [1]], [9, 0, 5], 0, 16, 4, 128),
+    _wl("rr_k_covers_chunks", [20, 18, 40], [[0, 1, 2]], [4], 32, 8, 2, 64),
+]
+
+
+@pytest.mark.parametrize("wl", RR, ids=[w.name for w in RR])
+@pytest.mark.parametrize("theta", [10000.0, 500000.0])
+def test_rerotation_variant(wl, theta):
+    """Re-rotation variant: every cached block of chunks 1.. is copied privately with
+    its K rotated by the chunk's linked offset (one bf16 step of the float64 oracle
+    at most); V, chunk 0 and the recomputed rows bit-exact; output and lse to the
+    usual bars against the oracle's re-rotated link step; shared blocks untouched."""
+    st = _stage(wl, rerotate_theta=theta)
+    st.run()
+    check_stage(st, rerotate_theta=theta)
+
+
+def test_rerotation_c5_long_context_sampled():
+    """The long-context workload (64 x 2048 + 256, k = 32) with re-rotation, Llama-3's
+    rotary base: linked offsets up to 129 024 (float64 angles)."""
+    st = _stage(get_config("c5", k=32), rerotate_theta=500000.0)
+    st.run()
+    check_stage(st, sample=_sample_rows, rerotate_theta=500000.0)

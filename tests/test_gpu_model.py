@@ -68,7 +68,7 @@ def _linked_rows(st, layer, s_pos):
     return _f64(K[s_pos]), _f64(V[s_pos])
 
 
-def _check(st, n_layers, caches_ref):
+def _check(st, n_layers, caches_ref, rerotate=False):
     wl = st.wl
     torch.cuda.synchronize()
     s_pos = oracle.legolink_positions(wl.chunk_lens, wl.suffix_len, wl.k)
@@ -76,7 +76,7 @@ def _check(st, n_layers, caches_ref):
     ws, fn = _oracle_inputs(wl, n_layers)
     emb = _s_embeddings(wl, s_pos)
     _, out_ref, kv_ref = oracle.link_model(emb, wl.chunk_lens, wl.suffix_len, wl.k, ws, fn, caches_ref,
-                                           bf16_storage=True, **_dims(wl))
+                                           bf16_storage=True, rerotate=rerotate, **_dims(wl))
     out = st.out.double().cpu().numpy()
     assert np.all(np.isfinite(out))
     err = np.abs(out - out_ref).max()
@@ -228,3 +228,29 @@ def test_recompute_all_wide_output_tiles():
     err = np.abs(st.out.double().cpu().numpy() - full).max()
     print(f"[gpu-test] fr_wide: final hidden max|err| {err:.3e}", flush=True)
     assert err <= ATOL, err
+
+
+@pytest.mark.parametrize("wl", [_small("rr_ragged_d64", [37, 100, 16, 51], 23, 5),
+                                _small("rr_k0_d128", [64, 45, 80], 30, 0, hidden=512, ffn=1536, hq=4, hkv=2, d=128)],
+                         ids=["rr_ragged_d64", "rr_k0_d128"])
+def test_compile_and_link_with_rerotation(wl):
+    """Re-rotation variant at model level: each side compiles the chunks, then links
+    with the cached K of chunks 1.. moved to its linked positions (the model's rotary
+    base); end-to-end parity, and the re-rotated linked cache of every layer within a
+    bf16 step of the oracle's."""
+    st = _stage(wl, caches="compile", rerotate=True)
+    st.run()
+    torch.cuda.synchronize()
+    ref = _oracle_compiled_caches(wl, wl.n_layers)
+    err = _check(st, wl.n_layers, ref, rerotate=True)
+    from paper_2410_15332_amd import epic_link as el
+    offs = oracle.chunk_offsets(wl.chunk_lens)
+    s_pos = oracle.legolink_positions(wl.chunk_lens, wl.suffix_len, wl.k)
+    for layer in range(wl.n_layers):
+        K, _ = el.read_linked_kv(_bits(st.k_caches[layer]), _bits(st.v_caches[layer]), st.views, 0)
+        rot = oracle.rerotate_cached(ref[layer][0], wl.chunk_lens, wl.rope_theta)
+        for j in range(1, len(wl.chunk_lens)):
+            rows = [t for t in range(wl.chunk_lens[j]) if offs[j] + t not in set(s_pos.tolist())]
+            got = _f64(K[[offs[j] + t for t in rows]])
+            assert np.abs(got - rot[j][rows]).max() <= ATOL, f"layer {layer} chunk {j}: re-rotated K"
+    print(f"[gpu-test] {wl.name} re-rotated: final hidden max|err| {err:.3e}", flush=True)

@@ -438,3 +438,69 @@ def test_dummy_compile_equals_link_after_cached_dummies():
         np.testing.assert_allclose(v1, v2, atol=1e-10, rtol=0)
     _, kv0 = oracle.compile_chunk(emb, ws, fn, bf16_storage=False, **TINY)
     assert np.abs(kv0[0][0] - kv[0][0]).max() > 1e-3
+
+
+def test_rerotated_naive_equals_causal_attention_at_linked_positions():
+    """Re-rotation variant: chunk caches hold K rotated at the chunk's own positions
+    0..L-1.  Rotating chunk j's rows by its linked offset must give K rotated at the
+    linked positions (so the rotations compose), and the k = 0 link step over them is
+    then ordinary causal attention with every key at its linked position (torch
+    SDPA).  Without re-rotation the same inputs give a different result."""
+    rng = np.random.default_rng(21)
+    lens, suf, hq, hkv, d, theta = [9, 13, 6], 5, 4, 2, 16, 10000.0
+    n = sum(lens) + suf
+    k_raw = rng.standard_normal((n, hkv, d))
+    v = rng.standard_normal((n, hkv, d))
+    q_raw = rng.standard_normal((n, hq, d))
+    offs = oracle.chunk_offsets(lens)
+    ck = [oracle.rope(k_raw[o:o + L], np.arange(L), theta) for o, L in zip(offs, lens)]
+    cv = [v[o:o + L] for o, L in zip(offs, lens)]
+    rot = oracle.rerotate_cached(ck, lens, theta, bf16_storage=False)
+    for o, L, r in zip(offs, lens, rot):
+        np.testing.assert_allclose(r, oracle.rope(k_raw[o:o + L], np.arange(o, o + L), theta), rtol=0, atol=1e-12)
+    k_lin = oracle.rope(k_raw, np.arange(n), theta)
+    q_lin = oracle.rope(q_raw, np.arange(n), theta)
+    s = np.arange(sum(lens), n)
+    # the rounding step of the stored variant is the only difference from the exact one
+    s_pos, out, _, K, _ = oracle.link_attention(lens, suf, 0, ck, cv, q_lin[s], k_lin[s], v[s],
+                                                rerotate_theta=theta)
+    assert np.abs(K[:sum(lens)] - k_lin[:sum(lens)]).max() < 2e-2
+    _, out_exact, _, _, _ = oracle.link_attention(lens, suf, 0, rot, cv, q_lin[s], k_lin[s], v[s])
+    G = hq // hkv
+    qt = torch.from_numpy(q_lin).permute(1, 0, 2)[None]
+    Kt = torch.from_numpy(k_lin).permute(1, 0, 2).repeat_interleave(G, dim=0)[None]
+    Vt = torch.from_numpy(v).permute(1, 0, 2).repeat_interleave(G, dim=0)[None]
+    ref = torch.nn.functional.scaled_dot_product_attention(qt, Kt, Vt, is_causal=True)[0].permute(1, 0, 2).numpy()
+    np.testing.assert_allclose(out_exact, ref[s], rtol=0, atol=1e-12)
+    assert np.abs(out - ref[s]).max() < 2e-2
+    _, out_plain, _, _, _ = oracle.link_attention(lens, suf, 0, ck, cv, q_lin[s], k_lin[s], v[s])
+    assert np.abs(out_plain - ref[s]).max() > 1e-2
+
+
+def test_rerotated_cache_equals_compile_at_linked_positions():
+    """Model level: a chunk compiled alone at positions off..off+L-1 has the same hidden
+    states as at 0..L-1 (rotary attention sees relative positions only) and K rotated
+    by off more; the HuggingFace forward at shifted position ids gives exactly the
+    re-rotated cache.  And the model-level link step with re-rotation and k = 0 runs
+    the suffix over those caches."""
+    ws, fn = _tiny_weights(2)
+    lens, suf = [7, 10], 3
+    emb = _tok_emb(sum(lens) + suf, seed=23)
+    caches = _compile_all(ws, fn, lens, emb, bf16=False)
+    m = _hf_model(ws, fn)
+    off = lens[0]
+    with torch.no_grad():
+        r = m(inputs_embeds=torch.from_numpy(emb[off:off + lens[1]])[None],
+              position_ids=torch.arange(off, off + lens[1])[None], use_cache=True)
+    for layer in range(2):
+        rot = oracle.rerotate_cached(caches[layer][0], lens, TINY["theta"], bf16_storage=False)
+        hk = r.past_key_values.layers[layer].keys[0].permute(1, 0, 2).numpy()
+        np.testing.assert_allclose(rot[1], hk, atol=2e-5, rtol=0)
+        np.testing.assert_array_equal(rot[0], caches[layer][0][0])
+    # with re-rotated caches every key sits at its linked position; the suffix rows of
+    # the k = 0 link step then equal a link over caches compiled at the linked positions
+    rot_caches = [(oracle.rerotate_cached(ck, lens, TINY["theta"], bf16_storage=False), cv) for ck, cv in caches]
+    s, out_r, _ = oracle.link_model(emb[17:], lens, suf, 0, ws, fn, caches, bf16_storage=False, rerotate=True,
+                                    **TINY)
+    _, out_e, _ = oracle.link_model(emb[17:], lens, suf, 0, ws, fn, rot_caches, bf16_storage=False, **TINY)
+    np.testing.assert_allclose(out_r, out_e, atol=1e-12, rtol=0)

@@ -380,3 +380,58 @@ def test_compile_plan_errors():
     assert e.value.status == 1
     s, _, v = el.epic_plan_compile([], [], 4, cfg, [], 8)    # nothing to compile
     assert s.n_s == 0 and s.n_private == 0
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_rerotation_plan(seed):
+    """rerotate = 1: every block of chunks 1.. becomes private; a block that keeps a
+    cached row copies its chunk block with priv_rot = the chunk's linked offset; chunk
+    0 stays shared; S, positions and linked layout are those of the plain plan."""
+    rng = np.random.default_rng(500 + seed)
+    reqs, n_used = _random_requests(rng, int(rng.integers(1, 4)))
+    for r in reqs:
+        if r.k < 0:
+            r.k = 3
+    rr = [el.Request(r.chunk_lens, r.chunk_blocks, r.suffix_len, r.k, True) for r in reqs]
+    cfg = el.attn_cfg(8, 2, 64)
+    need = el.epic_plan_sizes_get(rr, cfg, 1 << 30).n_private
+    free = list(range(n_used, n_used + need))
+    s0, _, v0 = el.epic_plan_link(reqs, cfg, list(range(n_used, n_used + need)), n_used + need)
+    s1, _, v1 = el.epic_plan_link(rr, cfg, free, n_used + need)
+    _check_linked(v1, len(rr))
+    assert v1["s_pos"].tolist() == v0["s_pos"].tolist() and v1["block_pos0"].tolist() == v0["block_pos0"].tolist()
+    assert not v0["priv_rot"].any() and s0.n_rerotated == 0
+    pv = {int(b): i for i, b in enumerate(v1["priv_block"])}
+    n_rot = 0
+    for b, r in enumerate(rr):
+        lb = v1["blk_off"][b]
+        offs = oracle.chunk_offsets(r.chunk_lens)
+        for j, (L, blocks) in enumerate(zip(r.chunk_lens, r.chunk_blocks)):
+            sel = 0 if j == 0 else min(r.k, L)
+            for i, cb in enumerate(blocks):
+                phys = int(v1["linked_blocks"][lb])
+                lb += 1
+                if j == 0:
+                    assert phys == cb
+                    continue
+                assert phys in pv and phys not in [x for bl in r.chunk_blocks for x in bl]
+                p = pv[phys]
+                keeps = sel < i * 16 + min(16, L - i * 16)
+                assert v1["priv_src"][p] == (cb if keeps else -1)
+                assert v1["priv_rot"][p] == (offs[j] if keeps else 0)
+                n_rot += int(keeps)
+    assert s1.n_rerotated == n_rot == int((v1["priv_rot"] != 0).sum())
+
+
+def test_rerotation_is_ignored_for_recompute_all_and_checked():
+    cfg = el.attn_cfg(8, 8, 64)
+    a = el.epic_plan_link([el.Request([20, 30], [[0, 1], [2, 3]], 4, -1, True)], cfg, list(range(4, 12)), 12)
+    b = el.epic_plan_link([el.Request([20, 30], [[0, 1], [2, 3]], 4, -1)], cfg, list(range(4, 12)), 12)
+    assert np.array_equal(a[1], b[1]) and a[0].n_rerotated == 0
+    req = el.Request([20, 30], [[0, 1], [2, 3]], 4, 0, True)
+    s = el.epic_plan_sizes_get([req], cfg, 10)
+    assert s.n_private == 2 + 1 and s.n_rerotated == 2
+    req.rerotate = 2
+    with pytest.raises(el.EpicError) as e:
+        el.epic_plan_sizes_get([req], cfg, 10)
+    assert e.value.status == 1
