@@ -439,6 +439,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5k32", choices=sorted(WORKLOADS))
     ap.add_argument("--split-blocks", type=int, default=0, help="override the planner's split-KV size")
+    ap.add_argument("--tile-rows", type=int, default=0, choices=(0, 128, 256),
+                    help="override the planner's attention tile size (rows = S rows x query heads)")
     ap.add_argument("--cpu-rows", type=int, default=640, help="S rows in the CPU-oracle sample (about 12 s on 16 cores)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -474,7 +476,8 @@ def main():
         return
     t0 = time.time()
     rr_theta = 500000.0 if args.workload.endswith("rr") else 0.0
-    st = harness.stage_attention(wl, device="cuda", split_blocks=args.split_blocks, rerotate_theta=rr_theta)
+    st = harness.stage_attention(wl, device="cuda", split_blocks=args.split_blocks, rerotate_theta=rr_theta,
+                                 tile_rows=args.tile_rows)
     torch.cuda.synchronize()
     log(f"staged {wl.name}: n_s={st.sizes.n_s} tiles={st.sizes.n_tiles} work={st.sizes.n_work} "
         f"partials={st.sizes.n_partials} private={st.sizes.n_private} re-rotated={st.sizes.n_rerotated} "

@@ -105,7 +105,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wv % SH::WAVES_M, wn = wv / SH::WAVES_M;   // wavefront tile: rows wm*WM.., columns wn*64..
+  // wavefront tile: rows wm*WM.., columns wn*64..  At TN = 128 the two wavefronts of
+  // each SIMD (wavefronts w and w + 4) take different row halves, so a tile whose
+  // rows past M leave half the wavefronts idle still keeps every SIMD busy.
+  const int wm = TN == 128 ? wv >> 1 : wv % SH::WAVES_M;
+  const int wn = TN == 128 ? wv & 1 : wv / SH::WAVES_M;
   const int w = blockIdx.x;
   const int wr = p.G % 8 == 0 ? (w % 8) * (p.G / 8) + w / 8 : w;   // XCD-contiguous worker index
   const int64_t su = p.sk_units;
@@ -148,6 +152,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   // ---- buffer->LDS loads: wavefronts 0..3 stage the 16 A row groups (4 each),
   // 4..7 the TN / 16 W row groups (NLB each).
   const bool a_wave = wv < 4;
+  // With M <= 128 (one row tile) the A row groups 8..15 hold no row of A: their
+  // loading wavefronts issue nothing (none of their waits then has anything to wait for).
+  const bool dma_idle = TN == 128 && a_wave && g.M <= 128 && wv >= 2;
   const int nl = a_wave ? 4 : SH::NLB;                     // loads per stage of this wavefront
   const int grp0 = nl * (wv & 3);
   const int lrow = lane >> 2;                              // row within a 16-row group
@@ -174,6 +181,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   char* const dma_base = a_wave ? lds.a[0] + grp0 * 1024 : lds.b[0] + grp0 * 1024;
   const int dma_stage = a_wave ? SH::A_STAGE : SH::B_STAGE;
   auto dma = [&](int buf, int kt) __attribute__((always_inline)) {
+    if (dma_idle) return;
     char* dst = dma_base + buf * dma_stage;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -243,19 +251,31 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
       const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(g.C, 0, g.M * g.N * 4, kBufWord3);
       const int n = nt * TN + wn * 64 + col;
 #pragma unroll
-      for (int ii = 0; ii < CT / J; ++ii)
+      for (int ii = 0; ii < CT / J; ++ii) {
+        // residual: every load of the row block first, so they are in flight together
+        // (a load may not move above an earlier store through the same descriptor)
+        float cin[16][J];
+        if constexpr (EPI == kResidual) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int m = m0 + (h * (CT / J) + ii) * 32 + (r >> 2) * 8 + (r & 3);
+#pragma unroll
+            for (int j = 0; j < J; ++j)
+              cin[r][j] = __builtin_bit_cast(float,
+                                             __builtin_amdgcn_raw_buffer_load_b32(ro, (m * g.N + n + j * 32) * 4, 0, 0));
+          }
+        }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int m = m0 + (h * (CT / J) + ii) * 32 + (r >> 2) * 8 + (r & 3);
 #pragma unroll
           for (int j = 0; j < J; ++j) {
-            const int off = (m * g.N + n + j * 32) * 4;
             float x = v[ii * J + j][r];
-            if constexpr (EPI == kResidual)
-              x += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ro, off, 0, 0));
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), ro, off, 0, 0);
+            if constexpr (EPI == kResidual) x += cin[r][j];
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), ro, (m * g.N + n + j * 32) * 4, 0, 0);
           }
         }
+      }
     }
   };
 
@@ -265,6 +285,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   auto finish = [&](const Cursor& c) __attribute__((always_inline)) {
     int mt, nt;
     tile_mn(c.tile, mt, nt);
+    if (TN == 128 && mt * kTM + wm * SH::WM >= g.M) return;   // every row of this part is past M: nothing to write
     if (c.kbeg == 0 && c.kend == p.ks) {
 #pragma unroll
       for (int h = 0; h < NCH; ++h) {
@@ -361,25 +382,44 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   Frags f0, f1;
   read(f0, 0, 0);
   zero_acc();
+  // rows of this wavefront's part of the current tile exist (else it only stages and
+  // syncs); only the 128-column tiles of short row sets skip (256-column tiles run
+  // when there are many row tiles, where the saving is small)
+  auto live_in = [&](int tile) __attribute__((always_inline)) {
+    if constexpr (TN != 128) return true;
+    int mt, nt;
+    tile_mn(tile, mt, nt);
+    return __builtin_amdgcn_readfirstlane(int(mt * kTM + wm * SH::WM < g.M)) != 0;
+  };
+  bool live = live_in(cc.tile);
   int u = 0, buf = 0;
   while (true) {
     // the units of one segment (the epilogue stays out of the hot loop)
     for (const int ue = u + (cc.kend - cc.kt); u < ue; ++u) {
       const int nbuf = buf + 1 == NS ? 0 : buf + 1;
-      read(f1, buf, 1);
-      mma(f0);
+      if (live) {
+        read(f1, buf, 1);
+        mma(f0);
+      }
       if (a_wave) wait_vmem<(NS - 2) * 4>();        // this wavefront's loads of unit u + 1
       else wait_vmem<(NS - 2) * SH::NLB>();
       barrier_lds();
       dma_next(buf);
-      read(f0, nbuf, 0);
-      mma(f1);
+      if (live) {
+        read(f0, nbuf, 0);
+        mma(f1);
+      }
       buf = nbuf;
     }
     finish(cc);
     if (u >= n_units) break;
     zero_acc();
     seek(cc, u);
+    const bool was_live = live;
+    live = live_in(cc.tile);
+    // f0 (first k-slice of unit u, in buffer buf: loaded and published at the last
+    // barrier) was only prefetched if the previous segment was live
+    if (live && !was_live) read(f0, buf, 0);
   }
   wait_vmem<0>();                       // no load may land in LDS after the workgroup ends
 }
