@@ -59,6 +59,32 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def ttft_medians(run, reps: int, evict_mib: int = 1024):
+    """Median link-step time of `reps` single runs (HIP events around each): warm
+    (back to back) and cold (each run after a write of evict_mib MiB on the same
+    stream, more than L2 plus the 256 MB MALL, so caches and operands start in HBM).
+    Taken after the timed region; the timed region itself is the K-step mean."""
+    import numpy as np
+    import torch
+
+    evict = torch.empty(evict_mib * (1 << 20) // 4, dtype=torch.float32, device="cuda")
+    out = {}
+    for kind in ("warm", "cold"):
+        times = []
+        for _ in range(reps):
+            if kind == "cold":
+                evict.fill_(1.0)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            run()
+            b.record()
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        out[kind] = float(np.median(times))
+    del evict
+    return out
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for f in ("attention.hip", "device_common.h", "kernels.h"):
@@ -355,6 +381,8 @@ def bench_model(args, wl, n_dummy: int = 0):
     achieved = total / (step_ms * 1e-3) / 1e12
     log(f"step {step_ms:.3f} ms; layer attention {attn_ms:.4f} ms ({attn_flops / attn_ms / 1e9:.1f} TFLOP/s); "
         f"all layers {achieved:.1f} TFLOP/s")
+    med = {"warm": float("nan"), "cold": float("nan")} if args.no_ttft_medians else ttft_medians(st.run, max(K, 20))
+    log(f"median of {max(K, 20)} single runs: warm {med['warm']:.3f} ms, cold {med['cold']:.3f} ms")
     result = {
         "metric": METRIC, "value": round(n_s / (step_ms * 1e-3), 1), "unit": "recomputed tokens/s", "n_gpus": 1,
         "steps": K, "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True,
@@ -367,6 +395,8 @@ def bench_model(args, wl, n_dummy: int = 0):
                    "linked_tokens": int(st.sizes.max_pos),
                    "parallelism": "single GPU"},
         "ttft_ms": round(step_ms, 4),
+        "ttft_warm_median_ms": None if args.no_ttft_medians else round(med["warm"], 4),
+        "ttft_cold_median_ms": None if args.no_ttft_medians else round(med["cold"], 4),
         "attention_tflops": round(attn_flops / attn_ms / 1e9, 2),
         "model_tflops": round(achieved, 2),
         "roofline": {"bound": "mfma", "kernel": "whole link step (GEMMs + attention)", "achieved": round(achieved, 2),
@@ -441,8 +471,11 @@ def main():
     ap.add_argument("--split-blocks", type=int, default=0, help="override the planner's split-KV size")
     ap.add_argument("--tile-rows", type=int, default=0, choices=(0, 128, 256),
                     help="override the planner's attention tile size (rows = S rows x query heads)")
-    ap.add_argument("--cpu-rows", type=int, default=640, help="S rows in the CPU-oracle sample (about 12 s on 16 cores)")
+    ap.add_argument("--cpu-rows", type=int, default=1024, help="S rows in the CPU-oracle sample (about 13 s on 16 cores)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ttft-medians", action="store_true",
+                    help="skip the warm / cold single-run medians after the timed region (profiling runs, "
+                         "so every launch of a kernel belongs to the warm-up or the timed steps)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="before the timed region, run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -520,6 +553,8 @@ def main():
     achieved = flops / (attn_ms * 1e-3) / 1e12
     log(f"step {step_ms:.4f} ms (wall {wall / K * 1e3:.4f} ms): write {write_ms:.4f} attn {attn_ms:.4f} "
         f"combine {comb_ms:.4f}; attention {achieved:.1f} TFLOP/s")
+    med = {"warm": float("nan"), "cold": float("nan")} if args.no_ttft_medians else ttft_medians(st.run, max(K, 20))
+    log(f"median of {max(K, 20)} single runs: warm {med['warm']:.4f} ms, cold {med['cold']:.4f} ms")
 
     traffic = traffic_from_profile(args.workload)
     result = {
@@ -552,6 +587,8 @@ def main():
             "parallelism": "single GPU",
         },
         "ttft_ms": round(step_ms, 5),
+        "ttft_warm_median_ms": None if args.no_ttft_medians else round(med["warm"], 5),
+        "ttft_cold_median_ms": None if args.no_ttft_medians else round(med["cold"], 5),
         "attention_tflops": round(achieved, 2),
         "attention_incl_combine_tflops": round(flops / ((attn_ms + comb_ms) * 1e-3) / 1e12, 2),
         "kernel_ms": {"link_write": round(write_ms, 5), "attention": round(attn_ms, 5),
