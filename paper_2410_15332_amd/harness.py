@@ -393,3 +393,23 @@ def gemm_flops_per_layer(wl, n_rows: int) -> float:
     """2 * rows * (sum of in * out over the layer's weight matrices)."""
     qkv = (wl.num_q_heads + 2 * wl.num_kv_heads) * wl.head_dim
     return 2.0 * n_rows * wl.hidden * (qkv + wl.num_q_heads * wl.head_dim + 3 * wl.ffn)
+
+
+def capture_graph(run):
+    """Capture one call of `run` (a staged step that allocates nothing and launches
+    only kernels and device copies on the current stream) into a HIP graph; returns
+    the torch graph object, whose replay() reruns the step.  One eager call on a side
+    stream first, as graph capture expects warmed-up work."""
+    import torch
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run()
+    torch.cuda.synchronize()
+    return graph
