@@ -15,6 +15,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build", "epic_link")
 LIB = os.path.join(PKG, "libepic_link.so")
+# measurement tooling, outside the product library: the MFMA throughput probe
+PROBE_SRC = os.path.join(PKG, "probe", "mfma_peak.hip")
+PROBE_LIB = os.path.join(PKG, "probe", "libepic_probe.so")
 
 SOURCES = ["status.cpp", "plan.cpp", "api.cpp", "model.cpp", "link_write.hip", "attention.hip", "gemm.hip",
            "layer.hip"]
@@ -48,8 +51,14 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
+    tmp = PROBE_LIB + ".tmp"
+    cmd = [HIPCC, "-x", "hip", f"--offload-arch={ARCH}", *DEVICE_FLAGS, *COMMON, "-shared", PROBE_SRC, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"probe build failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, PROBE_LIB)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {PROBE_LIB}")
     return LIB
 
 
