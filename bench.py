@@ -472,7 +472,7 @@ def bench_decode(args, wl):
     from paper_2410_15332_amd import epic_link as el
     from paper_2410_15332_amd import harness
 
-    st = harness.stage_attention(wl, device="cuda", spare_blocks=4 * wl.batch)
+    st = harness.stage_attention(wl, device="cuda", spare_blocks=4 * wl.batch, split_blocks=args.split_blocks)
     st.run()
     ds = harness.stage_decode(wl, st.cfg, st.sizes, st.dplan.host, st.spare, st.num_blocks, [1] * wl.batch)
     torch.cuda.synchronize()
@@ -507,7 +507,9 @@ def bench_decode(args, wl):
                    "num_kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim,
                    "linked_tokens_per_request": int(linked.max()), "parallelism": "single GPU"},
         "kernel_ms": {"attention": round(attn_ms, 5), "combine": round(comb_ms, 5)},
-        "roofline": {"bound": "hbm", "kernel": f"link_attention_kernel<{wl.head_dim}, {ds.sizes.tile_rows // 32}>",
+        "roofline": {"bound": "hbm",
+                     "kernel": (f"link_decode_kernel<{wl.head_dim}>" if ds.sizes.tile_rows == 16
+                                else f"link_attention_kernel<{wl.head_dim}, {ds.sizes.tile_rows // 32}>"),
                      "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "algorithmic_bytes_per_launch": kv_bytes, "traffic": None},
     }

@@ -63,8 +63,10 @@ const char* epic_version(void);
  * softmax_scale == 0 means 1 / sqrt(head_dim).
  * kv_split_blocks: key blocks per split-KV work item (0 = library default);
  * rows whose keys span several work items are merged with a log-sum-exp combine.
- * tile_rows: query rows (S row x head) per attention workgroup, 128 or 256
- * (0 = library default: 256 when the rows of a tile need nearly the same keys).
+ * tile_rows: query rows (S row x head) per attention workgroup, 16, 128 or 256
+ * (0 = library default: 16 when every request has at most 16 / G S rows, as in
+ * decode; else 256 when the rows of a tile need nearly the same keys, else 128).
+ * 16-row tiles need G <= 16.
  * rope_theta: the rotary base theta (inverse frequency theta^(-2i/D), pairs (i, i + D/2))
  * that cached K was rotated with; a plan with re-rotated blocks needs it > 0. */
 typedef struct {
@@ -109,7 +111,7 @@ typedef struct {
   int32_t n_tiles;          /* attention query tiles (per KV head) */
   int32_t n_work;           /* attention work items (per KV head) */
   int32_t n_partials;       /* split-KV partial results (per KV head) */
-  int32_t tile_rows;        /* query rows (S row x head) per tile: 128 or 256 */
+  int32_t tile_rows;        /* query rows (S row x head) per tile: 16, 128 or 256 */
   int32_t max_pos;          /* 1 + largest linked position in the batch */
   int32_t n_rerotated;      /* private blocks whose copied rows are re-rotated */
   int64_t total_ints;       /* int32 entries of the plan buffer */

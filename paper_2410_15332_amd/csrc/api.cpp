@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdint>
 
+#include "decode_attention.h"
 #include "kernels.h"
 #include "link_write.h"
 #include "plan_internal.h"
@@ -28,8 +29,8 @@ epic_status check_plan(const epic_plan_sizes* s, const epic_plan* p) {
   EPIC_CHECK_ARG(s != nullptr, "plan sizes are NULL");
   EPIC_CHECK_ARG(p != nullptr, "device plan is NULL");
   EPIC_CHECK_ARG(s->n_s >= 0 && s->n_work >= 0 && s->n_partials >= 0 && s->n_private >= 0, "bad plan sizes");
-  EPIC_CHECK_ARG(valid_tile_rows(s->tile_rows), "plan tile rows %d (expected %d or %d)", s->tile_rows,
-                 kTileRowsSmall, kTileRowsLarge);
+  EPIC_CHECK_ARG(valid_tile_rows(s->tile_rows), "plan tile rows %d (expected %d, %d or %d)", s->tile_rows,
+                 kTileRowsTiny, kTileRowsSmall, kTileRowsLarge);
   if (s->n_s > 0)
     EPIC_CHECK_ARG(p->s_pos && p->linked_blocks && p->block_pos0 && p->block_len && p->tiles && p->work,
                    "device plan arrays are NULL");
@@ -104,7 +105,10 @@ epic_status run_link_attention(const epic_attn_cfg* cfg, const epic_plan_sizes* 
   const float scale = cfg->softmax_scale > 0.0f ? cfg->softmax_scale : 1.0f / std::sqrt(float(cfg->head_dim));
   a.scale_log2 = scale * kLog2eHost;
   record_event(1, stream);
-  launch_link_attention(a, cfg->head_dim, s->n_work, stream);
+  if (s->tile_rows == kTileRowsTiny)
+    launch_link_decode(a, cfg->head_dim, s->n_work, stream);
+  else
+    launch_link_attention(a, cfg->head_dim, s->n_work, stream);
   record_event(2, stream);
   if (s->n_partials > 0) launch_link_combine(a, cfg->head_dim, s->n_tiles, stream);
   record_event(3, stream);

@@ -32,8 +32,11 @@ epic_status validate_attn_cfg(const epic_attn_cfg* cfg) {
   if (cfg->kv_split_blocks < 0)
     return fail(EPIC_ERR_INVALID_ARG, "kv_split_blocks %d < 0", cfg->kv_split_blocks);
   if (cfg->tile_rows != 0 && !valid_tile_rows(cfg->tile_rows))
-    return fail(EPIC_ERR_UNSUPPORTED, "tile_rows %d (expected 0, %d or %d)", cfg->tile_rows, kTileRowsSmall,
-                kTileRowsLarge);
+    return fail(EPIC_ERR_UNSUPPORTED, "tile_rows %d (expected 0, %d, %d or %d)", cfg->tile_rows, kTileRowsTiny,
+                kTileRowsSmall, kTileRowsLarge);
+  if (cfg->tile_rows == kTileRowsTiny && G > kTileRowsTiny)
+    return fail(EPIC_ERR_UNSUPPORTED, "tile_rows %d needs at most %d query heads per KV head (%d)", kTileRowsTiny,
+                kTileRowsTiny, G);
   if (!(cfg->softmax_scale >= 0.0f)) return fail(EPIC_ERR_INVALID_ARG, "softmax_scale must be >= 0");
   return EPIC_OK;
 }
@@ -171,6 +174,7 @@ struct TileShape {
 };
 constexpr TileShape kShapeLarge{kTileRowsLarge, 256, 1.0, 3.0, 4.0};   // one 8-wavefront workgroup per CU, 256 CUs
 constexpr TileShape kShapeSmall{kTileRowsSmall, 512, 1.0, 2.0, 4.0};   // two 4-wavefront workgroups per CU
+constexpr TileShape kShapeTiny{kTileRowsTiny, 768, 1.0, 2.0, 1.0};      // three 4-wavefront workgroups per CU
 
 // Estimated duration of the attention launch for a split: the items (times the
 // KV heads, head-minor as in the grid) are dealt in launch order to the
@@ -259,6 +263,31 @@ void choose_tiles(const std::vector<ReqRows>& rr, const epic_attn_cfg* cfg, epic
                   std::vector<Tile>* tiles_out, int* split_out) {
   const int G = cfg->num_q_heads / cfg->num_kv_heads;
   std::vector<Tile>& tiles = *tiles_out;
+  // 16-row tiles (the decode kernel) when every request has at most 16 / G S rows:
+  // a 128-row tile would hold almost only empty rows
+  bool few_rows = G <= kTileRowsTiny;
+  size_t any_rows = 0;
+  for (const ReqRows& r : rr) {
+    few_rows = few_rows && r.pos.size() <= static_cast<size_t>(kTileRowsTiny / G);
+    any_rows += r.pos.size();
+  }
+  if (cfg->tile_rows == kTileRowsTiny || (cfg->tile_rows == 0 && few_rows && any_rows > 0)) {
+    make_tiles(rr, kTileRowsTiny / G, &tiles);
+    s->tile_rows = kTileRowsTiny;
+    double est = 0.0;
+    const int split = split_blocks(cfg, tiles, kShapeTiny, &est);
+    *split_out = split;
+    int64_t n_work = 0, n_part = 0;
+    for (const Tile& t : tiles) {
+      const int ns = std::max(1, cdiv(t.nblk, split));
+      n_work += ns;
+      if (ns > 1) n_part += ns;
+    }
+    s->n_tiles = static_cast<int32_t>(tiles.size());
+    s->n_work = static_cast<int32_t>(n_work);
+    s->n_partials = static_cast<int32_t>(n_part);
+    return;
+  }
   std::vector<Tile> small, large;
   make_tiles(rr, kTileRowsSmall / G, &small);
   make_tiles(rr, kTileRowsLarge / G, &large);

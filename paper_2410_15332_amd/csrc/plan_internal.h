@@ -10,7 +10,9 @@ constexpr int kBlock = 16;         // token slots per KV block
 // CU) or 256 (one 8-wavefront workgroup per CU), chosen per plan by the planner
 constexpr int kTileRowsSmall = 128;
 constexpr int kTileRowsLarge = 256;
-inline bool valid_tile_rows(int r) { return r == kTileRowsSmall || r == kTileRowsLarge; }
+// 16-row tiles: decode-shaped plans (a few S rows per request), own kernel
+constexpr int kTileRowsTiny = 16;
+inline bool valid_tile_rows(int r) { return r == kTileRowsTiny || r == kTileRowsSmall || r == kTileRowsLarge; }
 constexpr int kKvTileBlocks = 4;   // KV blocks staged per attention iteration (64 keys)
 constexpr int kWorkInts = 8;       // int32 per attention work item
 constexpr float kLog2eHost = 1.442695040888963407f;

@@ -216,6 +216,25 @@ def test_forced_split_kv(split, tile_rows):
     check_stage(st)
 
 
+@pytest.mark.parametrize("wl", EDGE, ids=[w.name for w in EDGE])
+def test_edge_cases_16_row_tiles(wl):
+    """The decode kernel (16-row tiles) on general link steps: many tiles per request,
+    ragged blocks, split-KV pieces."""
+    st = _stage(wl, tile_rows=16)
+    assert st.sizes.tile_rows == 16
+    st.run()
+    check_stage(st)
+
+
+@pytest.mark.parametrize("split", [4, 8])
+def test_forced_split_kv_16_row_tiles(split):
+    wl = _wl("split16", [300, 211, 129], [[0, 1, 2]], [70], 24, 32, 8, 128)
+    st = _stage(wl, split_blocks=split, tile_rows=16)
+    assert st.sizes.n_partials > 0 and st.sizes.tile_rows == 16
+    st.run()
+    check_stage(st)
+
+
 def test_empty_selection_launches_nothing():
     wl = _wl("empty", [40, 40], [[0, 1]], [0], 0, 8, 8, 64)
     st = _stage(wl)

@@ -29,10 +29,11 @@ def _f64(bits):
     return synth.bf16_bits_to_f32(bits).astype(np.float64)
 
 
-def _run_decode(wl, steps, spare_blocks=64):
+def _run_decode(wl, steps, spare_blocks=64, tile_rows=0):
     from paper_2410_15332_amd import epic_link as el, harness
-    print(f"[gpu-test] decode after {wl.name} k={wl.k}: steps {[sum(s) for s in steps]} tokens", flush=True)
-    st = harness.stage_attention(wl, spare_blocks=spare_blocks)
+    print(f"[gpu-test] decode after {wl.name} k={wl.k}: steps {[sum(s) for s in steps]} tokens, "
+          f"tile rows {tile_rows or 'auto'}", flush=True)
+    st = harness.stage_attention(wl, spare_blocks=spare_blocks, tile_rows=tile_rows)
     st.run()
     hq, hkv, d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
     per = []
@@ -50,6 +51,10 @@ def _run_decode(wl, steps, spare_blocks=64):
     worst = 0.0
     for new in steps:
         ds = harness.stage_decode(wl, st.cfg, prev_sizes, prev_host, spare, st.num_blocks, new)
+        if tile_rows:
+            assert ds.sizes.tile_rows == tile_rows
+        elif max(new) <= 16 // (wl.num_q_heads // wl.num_kv_heads) and sum(new) > 0:
+            assert ds.sizes.tile_rows == 16, "decode-shaped plan without 16-row tiles"
         ds.run(st.k_cache, st.v_cache)
         torch.cuda.synchronize()
         out, lse = ds.out.float().cpu().numpy(), ds.lse.cpu().numpy()
@@ -88,8 +93,13 @@ def test_decode_after_c1():
     _run_decode(get_config("c1"), [[1], [3], [16], [0], [1]])
 
 
-def test_decode_after_c2_gqa():
-    _run_decode(get_config("c2"), [[1], [1], [17], [5]])
+@pytest.mark.parametrize("tile_rows", [0, 16, 128])
+def test_decode_after_c2_gqa(tile_rows):
+    """Auto: 16-row tiles (the decode kernel) for 1-token steps, 128-row tiles for 17
+    and 5 tokens at G = 4.  Forced 16: the link step itself and every decode step on
+    the decode kernel (several 16-row tiles per request).  Forced 128: the prefill
+    kernel throughout."""
+    _run_decode(get_config("c2"), [[1], [1], [17], [5]], tile_rows=tile_rows)
 
 
 def test_decode_batched_c4():

@@ -435,3 +435,23 @@ def test_rerotation_is_ignored_for_recompute_all_and_checked():
     with pytest.raises(el.EpicError) as e:
         el.epic_plan_sizes_get([req], cfg, 10)
     assert e.value.status == 1
+
+
+def test_decode_shaped_plans_use_16_row_tiles():
+    """A plan where every request has at most 16 / G S rows gets 16-row tiles (the
+    decode kernel); G above 16 cannot; the override is checked."""
+    cfg = el.attn_cfg(32, 8, 128)                       # G = 4
+    reqs = [el.Request([64], [[0, 1, 2, 3]], 3, 0), el.Request([], [], 4, 0)]
+    s, _, v = el.epic_plan_link(reqs, cfg, list(range(4, 12)), 12)
+    assert s.tile_rows == 16 and s.n_tiles == 2
+    assert v["tiles"].reshape(-1, 4)[:, 1].tolist() == [3, 4]
+    s, _, _ = el.epic_plan_link([el.Request([64], [[0, 1, 2, 3]], 5, 0)], cfg, list(range(4, 12)), 12)
+    assert s.tile_rows == 128                           # 5 rows > 16 / G
+    wide = el.attn_cfg(32, 1, 64)                       # G = 32
+    s, _, _ = el.epic_plan_link([el.Request([], [], 1, 0)], wide, [0], 4)
+    assert s.tile_rows == 128
+    with pytest.raises(el.EpicError) as e:
+        el.epic_plan_sizes_get([el.Request([], [], 1, 0)], el.attn_cfg(32, 1, 64, 0.0, 0, 16), 4)
+    assert e.value.status == 2
+    s = el.epic_plan_sizes_get([el.Request([], [], 40, 0)], el.attn_cfg(32, 8, 128, 0.0, 0, 16), 4)
+    assert s.tile_rows == 16 and s.n_tiles == 10        # forced: 4 S rows per tile
