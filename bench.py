@@ -461,6 +461,42 @@ def bench_model(args, wl, n_dummy: int = 0):
     print(json.dumps(result), flush=True)
 
 
+def cpu_baseline_decode(wl, st, ds, budget_s: float = 10.0):
+    """Time the float64 oracle's decode step (oracle.decode_attention, one new token)
+    request after request until about budget_s seconds have passed; tokens/s over
+    the requests timed (each request costs the same at these shapes)."""
+    import numpy as np
+
+    import oracle
+    import synth
+    from threadpoolctl import threadpool_info
+
+    hq, hkv, d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    f = lambda x: synth.bf16_bits_to_f32(x).astype(np.float64)  # noqa: E731
+    dt, n_req = 0.0, 0
+    for r, chunks in enumerate(wl.requests):
+        lens = [wl.chunk_lens[c] for c in chunks]
+        ck, cv = [], []
+        for c in chunks:
+            kb, vb = synth.chunk_cache(wl.seed, c, wl.chunk_lens[c], hkv, d, wl.value_scale, qk_scale=wl.qk_scale)
+            ck.append(f(kb))
+            cv.append(f(vb))
+        s_ref = oracle.legolink_positions(lens, wl.suffix_lens[r], wl.k)
+        _, k, v = synth.row_qkv(wl.seed, r, s_ref, hq, hkv, d, wl.value_scale, wl.qk_scale)
+        pos = ds.views["s_pos"][ds.views["s_off"][r]:ds.views["s_off"][r + 1]]
+        qn, kn, vn = (f(x) for x in synth.row_qkv(wl.seed, r, pos, hq, hkv, d, wl.value_scale, wl.qk_scale))
+        t0 = time.perf_counter()
+        oracle.decode_attention(lens, wl.suffix_lens[r], wl.k, ck, cv, f(k), f(v), qn, kn, vn)
+        dt += time.perf_counter() - t0
+        n_req += 1
+        if dt >= budget_s:
+            break
+    cores = max([x.get("num_threads", 1) for x in threadpool_info() if x.get("user_api") == "blas"] or [1])
+    return {"value": round(n_req / dt, 4), "unit": "decoded tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n_req} of {wl.batch} requests, one new token each, float64 NumPy oracle incl. K/V "
+                      f"expansion, {dt:.1f} s", "sample_seconds": round(dt, 2)}
+
+
 def bench_decode(args, wl):
     """Decode after the link step: one new token per request attends over its linked
     sequence (link step run once, untimed; the same decode step is then timed).  The
@@ -513,6 +549,9 @@ def bench_decode(args, wl):
                      "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "algorithmic_bytes_per_launch": kv_bytes, "traffic": None},
     }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle's decode step ...")
+        result["cpu_baseline"] = cpu_baseline_decode(wl, st, ds)
     print(json.dumps(result), flush=True)
 
 
