@@ -59,15 +59,18 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def mfma_probe_tflops(iters: int = 200000, blocks: int = 512, reps: int = 3):
+def mfma_probe_tflops(iters: int = 200000, blocks: int = 512, reps: int = 3, varied: bool = False):
     """bf16 MFMA rate this chip sustains: a probe kernel whose wavefronts issue only
-    independent 32x32x16 MFMAs (paper_2410_15332_amd/probe), best of `reps` launches."""
+    independent 32x32x16 MFMAs (paper_2410_15332_amd/probe), best of `reps` launches.
+    varied: operands with hashed signs and mantissas that change from one MFMA to the
+    next (the datapath toggles as with real data) instead of one fixed operand pair."""
     import ctypes
     import torch
 
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2410_15332_amd", "probe", "libepic_probe.so"))
-    lib.epic_probe_mfma_bf16.restype = ctypes.c_int
-    lib.epic_probe_mfma_bf16.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    fn = lib.epic_probe_mfma_bf16_varied if varied else lib.epic_probe_mfma_bf16
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
     lib.epic_probe_mfma_bf16_flops.restype = ctypes.c_double
     lib.epic_probe_mfma_bf16_flops.argtypes = [ctypes.c_int, ctypes.c_int]
     out = torch.empty(blocks * 512, dtype=torch.float32, device="cuda")
@@ -76,7 +79,7 @@ def mfma_probe_tflops(iters: int = 200000, blocks: int = 512, reps: int = 3):
     for i in range(reps + 1):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
-        rc = lib.epic_probe_mfma_bf16(out.data_ptr(), blocks, iters, stream)
+        rc = fn(out.data_ptr(), blocks, iters, stream)
         b.record()
         torch.cuda.synchronize()
         if rc != 0:
@@ -664,8 +667,10 @@ def main():
     if gms is not None:
         log(f"the step replayed from a HIP graph: {gms:.4f} ms")
     probe = None if args.no_ttft_medians else mfma_probe_tflops()
+    probe_v = None if args.no_ttft_medians else mfma_probe_tflops(varied=True)
     if probe is not None:
-        log(f"MFMA probe: {probe:.1f} TFLOP/s bf16 sustained; attention at {achieved / probe:.1%} of it")
+        log(f"MFMA probe: {probe:.1f} TFLOP/s bf16 sustained with fixed operands, {probe_v:.1f} with operands "
+            f"that change every MFMA; attention at {achieved / probe:.1%} / {achieved / probe_v:.1%} of them")
 
     traffic = traffic_from_profile(args.workload)
     result = {
@@ -717,6 +722,8 @@ def main():
             "peak_measured": None if probe is None else round(probe, 1),
             "frac_of_measured_peak": None if probe is None else round(achieved / probe, 4),
             "peak_measured_by": "MFMA-only probe kernel (independent v_mfma_f32_32x32x16_bf16 chains on every SIMD)",
+            "peak_measured_varied_operands": None if probe_v is None else round(probe_v, 1),
+            "frac_of_measured_peak_varied_operands": None if probe_v is None else round(achieved / probe_v, 4),
         },
     }
     if not args.no_cpu_baseline:

@@ -12,20 +12,49 @@ namespace {
 
 constexpr int kChains = 4;    // independent accumulators per wavefront
 
+// lowbias32 integer hash (Wellons' published constants): well-mixed operand bits
+__device__ inline uint32_t mix32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+
+// kVaried = false: one fixed operand pair per lane (small bf16 values, only the low
+// mantissa bits differ between lanes).  kVaried = true: eight A and eight B fragments
+// per lane with hashed signs and mantissas (exponent fixed at 2^-11, so sums stay
+// finite), cycled so that every MFMA of a chain sees new operand bits, as matrix
+// products of real data do; iters is then a multiple of 8.
+template <bool kVaried>
 __global__ __launch_bounds__(512) void mfma_peak_kernel(float* out, int iters) {
   const int t = threadIdx.x;
-  bf16x8 a, b;
+  constexpr int NF = kVaried ? 8 : 1;
+  bf16x8 a[NF], b[NF];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {          // small bf16 values (exponent 2^-10), so sums stay finite
-    a[i] = short(0x3A80 + ((t + i) & 15));
-    b[i] = short(0x3A80 + ((t * 3 + i) & 15));
-  }
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (kVaried) {
+        const uint32_t id = ((blockIdx.x * 512u + unsigned(t)) * 16u + unsigned(f)) * 8u + unsigned(i);
+        const uint32_t h = mix32(id);
+        a[f][i] = short(0x3A00 | (h & 0x807Fu));
+        b[f][i] = short(0x3A00 | ((h >> 16) & 0x807Fu));
+      } else {                           // small bf16 values (exponent 2^-10), so sums stay finite
+        a[f][i] = short(0x3A80 + ((t + i) & 15));
+        b[f][i] = short(0x3A80 + ((t * 3 + i) & 15));
+      }
+    }
   f32x16 c[kChains];
 #pragma unroll
   for (int k = 0; k < kChains; ++k) c[k] = f32x16{};
-  for (int it = 0; it < iters; ++it) {
+  for (int it = 0; it < iters; it += NF) {
 #pragma unroll
-    for (int k = 0; k < kChains; ++k) c[k] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c[k], 0, 0, 0);
+    for (int u = 0; u < NF; ++u)
+#pragma unroll
+      for (int k = 0; k < kChains; ++k)
+        c[k] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(u + k) % NF], b[(u + 3 * k) % NF], c[k], 0, 0, 0);
   }
   float s = 0.0f;
 #pragma unroll
@@ -42,7 +71,15 @@ __global__ __launch_bounds__(512) void mfma_peak_kernel(float* out, int iters) {
 // Returns 0, or the HIP error code of the launch.
 extern "C" int epic_probe_mfma_bf16(float* out, int n_blocks, int iters, void* stream) {
   if (out == nullptr || n_blocks <= 0 || iters <= 0) return int(hipErrorInvalidValue);
-  mfma_peak_kernel<<<dim3(unsigned(n_blocks)), 512, 0, static_cast<hipStream_t>(stream)>>>(out, iters);
+  mfma_peak_kernel<false><<<dim3(unsigned(n_blocks)), 512, 0, static_cast<hipStream_t>(stream)>>>(out, iters);
+  return int(hipGetLastError());
+}
+
+// The same launch with operands whose bits change from one MFMA to the next (see
+// mfma_peak_kernel<true>); iters must be a positive multiple of 8.
+extern "C" int epic_probe_mfma_bf16_varied(float* out, int n_blocks, int iters, void* stream) {
+  if (out == nullptr || n_blocks <= 0 || iters <= 0 || iters % 8 != 0) return int(hipErrorInvalidValue);
+  mfma_peak_kernel<true><<<dim3(unsigned(n_blocks)), 512, 0, static_cast<hipStream_t>(stream)>>>(out, iters);
   return int(hipGetLastError());
 }
 
