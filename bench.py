@@ -89,6 +89,56 @@ def mfma_probe_tflops(iters: int = 200000, blocks: int = 512, reps: int = 3, var
     return best
 
 
+def hbm_copy_probe_gbs(mib: int = 2048, reps: int = 5):
+    """HBM rate of a plain device-to-device copy of `mib` MiB (torch's copy kernel),
+    counting bytes read plus bytes written; best of `reps` after a warm-up."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    best = 0.0
+    for i in range(reps + 1):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src)
+        b.record()
+        torch.cuda.synchronize()
+        if i > 0:
+            best = max(best, 2.0 * n * 4 / (a.elapsed_time(b) * 1e-3) / 1e9)
+    del src, dst
+    return best
+
+
+def hbm_read_probe_gbs(mib: int = 2048, reps: int = 5, blocks: int = 4096):
+    """HBM read rate of a streaming-read probe kernel (paper_2410_15332_amd/probe)
+    over a `mib` MiB buffer read once per launch; best of `reps` after a warm-up."""
+    import ctypes
+    import torch
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2410_15332_amd", "probe", "libepic_probe.so"))
+    fn = lib.epic_probe_hbm_read
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    nbytes = mib * (1 << 20)
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    out = torch.empty(blocks, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    best = 0.0
+    for i in range(reps + 1):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        rc = fn(src.data_ptr(), nbytes, out.data_ptr(), blocks, stream)
+        b.record()
+        torch.cuda.synchronize()
+        if rc != 0:
+            raise RuntimeError(f"HBM read probe launch failed: HIP error {rc}")
+        if i > 0:
+            best = max(best, nbytes / (a.elapsed_time(b) * 1e-3) / 1e9)
+    del src, out
+    return best
+
+
 def graph_step_ms(run, reps: int):
     """Mean step time of `reps` back-to-back replays of the step captured in a HIP
     graph (the same kernels; the launch gaps between them are gone)."""
@@ -564,6 +614,15 @@ def bench_decode(args, wl):
                      "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "algorithmic_bytes_per_launch": kv_bytes, "traffic": None},
     }
+    if not args.no_ttft_medians:
+        read_gbs = hbm_read_probe_gbs()
+        copy_gbs = hbm_copy_probe_gbs()
+        log(f"HBM probes: a streaming read of 2 GiB moves {read_gbs:.0f} GB/s, a 2 GiB device-to-device copy "
+            f"{copy_gbs:.0f} GB/s (read + write); decode attention at {gbs / read_gbs:.1%} of the read rate")
+        result["roofline"]["peak_measured"] = round(read_gbs, 1)
+        result["roofline"]["frac_of_measured_peak"] = round(gbs / read_gbs, 4)
+        result["roofline"]["peak_measured_by"] = "streaming-read probe kernel over 2 GiB (16-byte loads, grid stride)"
+        result["roofline"]["copy_measured"] = round(copy_gbs, 1)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle's decode step ...")
         result["cpu_baseline"] = cpu_baseline_decode(wl, st, ds)

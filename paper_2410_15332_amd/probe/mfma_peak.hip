@@ -64,6 +64,30 @@ __global__ __launch_bounds__(512) void mfma_peak_kernel(float* out, int iters) {
   out[size_t(blockIdx.x) * blockDim.x + t] = s;   // keeps the products live
 }
 
+// Streaming-read probe: every thread reads 16-byte words at a grid stride, four
+// loads in flight per trip, and folds them into one word per workgroup.
+__global__ __launch_bounds__(256) void hbm_read_kernel(const uint4* src, size_t n16, uint32_t* out) {
+  const size_t stride = size_t(gridDim.x) * 256;
+  size_t i = size_t(blockIdx.x) * 256 + threadIdx.x;
+  uint32_t acc = 0;
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+    acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^ d.z ^ d.w;
+  }
+  for (; i < n16; i += stride) {
+    const uint4 a = src[i];
+    acc ^= a.x ^ a.y ^ a.z ^ a.w;
+  }
+  __shared__ uint32_t red[256];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t x = 0;
+    for (int t = 0; t < 256; ++t) x ^= red[t];
+    out[blockIdx.x] = x;                  // keeps the loads live
+  }
+}
+
 }  // namespace
 
 // out: device buffer of n_blocks * 512 floats.  Launches n_blocks workgroups of 8
@@ -86,4 +110,14 @@ extern "C" int epic_probe_mfma_bf16_varied(float* out, int n_blocks, int iters, 
 // Flops of one launch.
 extern "C" double epic_probe_mfma_bf16_flops(int n_blocks, int iters) {
   return double(n_blocks) * 8.0 * double(iters) * kChains * 2.0 * 32 * 32 * 16;
+}
+
+// src: device buffer of `bytes` bytes (a multiple of 16); out: n_blocks words.
+// Launches n_blocks workgroups of 256 threads that read the whole buffer once.
+extern "C" int epic_probe_hbm_read(const void* src, size_t bytes, uint32_t* out, int n_blocks, void* stream) {
+  if (src == nullptr || out == nullptr || n_blocks <= 0 || bytes == 0 || bytes % 16 != 0)
+    return int(hipErrorInvalidValue);
+  hbm_read_kernel<<<dim3(unsigned(n_blocks)), 256, 0, static_cast<hipStream_t>(stream)>>>(
+      static_cast<const uint4*>(src), bytes / 16, out);
+  return int(hipGetLastError());
 }
