@@ -43,3 +43,23 @@ def test_workspace_bytes_scale_with_partials():
     s = el.epic_plan_sizes_get(reqs, cfg, 1000)
     assert s.n_partials > 0
     assert el.epic_link_workspace_bytes(cfg, s) >= s.n_partials * 8 * 128 * (128 + 1) * 4
+
+
+def test_probe_library_exports_what_bench_calls():
+    """The measurement probes (built beside the product library, never linked into
+    it) load without a GPU, export the entry points bench.py binds, and reject bad
+    arguments on the host before any launch."""
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2410_15332_amd", "probe", "libepic_probe.so"))
+    for name in ("epic_probe_mfma_bf16", "epic_probe_mfma_bf16_varied", "epic_probe_mfma_bf16_flops",
+                 "epic_probe_hbm_read"):
+        assert hasattr(lib, name), name
+    lib.epic_probe_mfma_bf16_flops.restype = ctypes.c_double
+    lib.epic_probe_mfma_bf16_flops.argtypes = [ctypes.c_int, ctypes.c_int]
+    assert lib.epic_probe_mfma_bf16_flops(2, 3) == 2 * 8 * 3 * 4 * 2.0 * 32 * 32 * 16
+    lib.epic_probe_mfma_bf16_varied.restype = ctypes.c_int
+    lib.epic_probe_mfma_bf16_varied.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    assert lib.epic_probe_mfma_bf16_varied(None, 1, 8, None) != 0          # no output buffer
+    lib.epic_probe_hbm_read.restype = ctypes.c_int
+    lib.epic_probe_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
+                                        ctypes.c_void_p]
+    assert lib.epic_probe_hbm_read(None, 16, None, 1, None) != 0            # no buffers
