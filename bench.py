@@ -615,6 +615,9 @@ def bench_decode(args, wl):
                      "algorithmic_bytes_per_launch": kv_bytes, "traffic": None},
     }
     if not args.no_ttft_medians:
+        gms = graph_step_ms(lambda: ds.run(st.k_cache, st.v_cache), K)
+        log(f"the decode step replayed from a HIP graph: {gms:.4f} ms")
+        result["step_graph_ms"] = round(gms, 5)
         read_gbs = hbm_read_probe_gbs()
         copy_gbs = hbm_copy_probe_gbs()
         log(f"HBM probes: a streaming read of 2 GiB moves {read_gbs:.0f} GB/s, a 2 GiB device-to-device copy "

@@ -61,3 +61,18 @@ def test_model_step_graph_replays():
     wl = ModelWorkload("graph_small", 41, 2, 512, 1024, 8, 2, 64, 16, 500000.0, 1e-5, [37, 100, 51], 23, 5)
     st = harness.stage_model(wl, caches="compile")
     _replays(st, lambda: [st.out, st.k_caches[1]], lambda: st.out.zero_())
+
+
+def test_decode_step_graph_replays():
+    """Decode after the link step (16-row tiles, split-KV partials and the combine)."""
+    import types
+
+    from paper_2410_15332_amd import harness
+    print("[gpu-test] graph: c2 decode step", flush=True)
+    wl = get_config("c2")
+    st = harness.stage_attention(wl, spare_blocks=4 * wl.batch)
+    st.run()
+    ds = harness.stage_decode(wl, st.cfg, st.sizes, st.dplan.host, st.spare, st.num_blocks, [1] * wl.batch)
+    assert ds.sizes.tile_rows == 16 and ds.sizes.n_partials > 0
+    step = types.SimpleNamespace(run=lambda: ds.run(st.k_cache, st.v_cache))
+    _replays(step, lambda: [ds.out, ds.lse, st.k_cache, st.v_cache], lambda: (ds.out.zero_(), ds.lse.zero_()))
