@@ -187,8 +187,10 @@ def ttft_medians(run, reps: int, evict_mib: int = 1024):
 
 
 def kernel_source_hash() -> str:
+    """Hash of what decides an attention launch's memory traffic: the kernel sources
+    and the planner that picks the kernel instance, tiles and split."""
     h = hashlib.sha256()
-    for f in ("attention.hip", "device_common.h", "kernels.h"):
+    for f in ("attention.hip", "device_common.h", "kernels.h", "plan.cpp", "plan_internal.h"):
         with open(os.path.join(ROOT, "paper_2410_15332_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -148,9 +148,12 @@ void make_tiles(const std::vector<ReqRows>& rr, int rows_per_tile, std::vector<T
   }
 }
 
-// Work items of a split, in launch order: segment-major (all first segments,
-// then all second segments, ...), and within a segment the tiles with the
-// longest key range first.  Each entry: (tile, segment).
+// Work items of a split, in launch order: longest key range first, so the
+// dispatcher's greedy fill of freed workgroup slots ends with the short items;
+// among equal lengths segment-major (all first segments, then all second
+// segments, ...) and tiles with the longest key range first, so workgroups that
+// start together read the same KV blocks through their XCD's L2.  Each entry:
+// (tile, segment).
 std::vector<std::pair<int, int>> item_order(const std::vector<Tile>& tiles, int split) {
   std::vector<int> order(tiles.size());
   for (size_t t = 0; t < tiles.size(); ++t) order[t] = static_cast<int>(t);
@@ -161,6 +164,11 @@ std::vector<std::pair<int, int>> item_order(const std::vector<Tile>& tiles, int 
   for (int seg = 0; seg < max_splits; ++seg)
     for (int t : order)
       if (seg < std::max(1, cdiv(tiles[t].nblk, split))) items.emplace_back(t, seg);
+  auto blocks = [&](const std::pair<int, int>& it) {
+    return std::min(tiles[it.first].nblk, (it.second + 1) * split) - it.second * split;
+  };
+  std::stable_sort(items.begin(), items.end(),
+                   [&](const std::pair<int, int>& x, const std::pair<int, int>& y) { return blocks(x) > blocks(y); });
   return items;
 }
 
@@ -255,10 +263,13 @@ namespace {
 
 // Tile size and split-KV split for these S rows; fills s->tile_rows, n_tiles,
 // n_work, n_partials.  256-row tiles share each staged K/V block between twice
-// the rows, which pays when their rows need the same keys: take them when they
-// cost at most 1% more (row x 64-key) steps than 128-row tiles -- rows of one
-// stretch of positions (recompute-all, suffix-only) rather than the first k rows
-// of several chunks -- and still give every CU a workgroup.
+// the rows, which pays when their rows need nearly the same keys and the tiles
+// still balance over the CUs.  Take them when they cost at most 5% more
+// (row x 64-key) steps than 128-row tiles, their estimated launch is at most
+// kLargeEdge times that of 128-row tiles (each estimate in its own kernel's
+// steps: the 8-wavefront kernel runs a 256-row step in about 1/1.07-1/1.13 of
+// the time two 4-wavefront workgroups take for two 128-row steps, measured), and
+// they give every CU a workgroup.
 void choose_tiles(const std::vector<ReqRows>& rr, const epic_attn_cfg* cfg, epic_plan_sizes* s,
                   std::vector<Tile>* tiles_out, int* split_out) {
   const int G = cfg->num_q_heads / cfg->num_kv_heads;
@@ -296,21 +307,25 @@ void choose_tiles(const std::vector<ReqRows>& rr, const epic_attn_cfg* cfg, epic
     for (const Tile& t : ts) n += int64_t(cdiv(t.nblk, kKvTileBlocks)) * rows;
     return n;
   };
-  double est = 0.0;
+  constexpr double kLargeEdge = 1.07;
+  double est = 0.0, est_small = 0.0;
   int split = split_blocks(cfg, large, kShapeLarge, &est);
   int64_t large_items = 0;
   for (const Tile& t : large) large_items += std::max(1, cdiv(t.nblk, split));
-  const bool use_large = cfg->tile_rows != 0
-                             ? cfg->tile_rows == kTileRowsLarge
-                             : row_steps(large, kTileRowsLarge) * 100 <= row_steps(small, kTileRowsSmall) * 101 &&
-                                   large_items * cfg->num_kv_heads >= kShapeLarge.slots;
+  bool use_large = cfg->tile_rows == kTileRowsLarge;
+  int split_small = 0;
+  if (cfg->tile_rows == 0 && row_steps(large, kTileRowsLarge) * 100 <= row_steps(small, kTileRowsSmall) * 105 &&
+      large_items * cfg->num_kv_heads >= kShapeLarge.slots) {
+    split_small = split_blocks(cfg, small, kShapeSmall, &est_small);
+    use_large = est <= kLargeEdge * est_small;
+  }
   if (use_large) {
     tiles.swap(large);
     s->tile_rows = kTileRowsLarge;
   } else {
     tiles.swap(small);
     s->tile_rows = kTileRowsSmall;
-    split = split_blocks(cfg, tiles, kShapeSmall, &est);
+    split = split_small > 0 ? split_small : split_blocks(cfg, tiles, kShapeSmall, &est);
   }
   *split_out = split;
   int64_t n_work = 0, n_part = 0;

@@ -201,11 +201,13 @@ def _long_request(lens, suffix, k):
 @pytest.mark.parametrize("lens,suffix,k,want", [
     ([2048] * 16, 256, -1, 256),   # recompute-all: every tile is one stretch of positions
     ([2048] * 64, 256, 0, 256),    # suffix only (Naive), split until every CU has a workgroup
-    ([2048] * 64, 256, 32, 128),   # first 32 rows of each chunk: 256-row tiles span two chunks
-    ([512] * 10, 64, 16, 128),     # small: 256-row tiles would leave CUs idle
+    ([2048] * 64, 256, 32, 256),   # first 32 rows of each chunk: tiles span two chunks (4% masked steps)
+    ([2048] * 64, 256, 4, 128),    # first 4 rows: 8 tiles per head balance worse than 16 (estimate)
+    ([512] * 10, 64, 16, 128),     # small: 256-row tiles waste 28% of the steps
 ])
 def test_tile_rows_default(lens, suffix, k, want):
-    """256-row tiles only when their rows need nearly the same keys and the launch fills the chip."""
+    """256-row tiles only when their rows need nearly the same keys, the launch fills the
+    chip, and the estimated launch (greedy dispatch of the items) is not clearly longer."""
     reqs, n = _long_request(lens, suffix, k)
     cfg, sizes, v, _ = _plan(reqs, n, 32, 8)
     assert sizes.tile_rows == want
