@@ -186,13 +186,27 @@ def ttft_medians(run, reps: int, evict_mib: int = 1024):
     return out
 
 
-def kernel_source_hash() -> str:
+def code_without_comments(text: str) -> str:
+    """C/C++ source with comments removed and whitespace runs collapsed (string
+    literals are kept as they are; these sources put no comment markers in them)."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return re.sub(r"\s+", " ", text).strip()
+
+
+def kernel_source_hash(sources=None) -> str:
     """Hash of what decides an attention launch's memory traffic: the kernel sources
-    and the planner that picks the kernel instance, tiles and split."""
+    and the planner that picks the kernel instance, tiles and split (code only, so an
+    edit of comments keeps a profile valid).  sources: {file name: text} to hash
+    instead of the files in the tree."""
     h = hashlib.sha256()
     for f in ("attention.hip", "device_common.h", "kernels.h", "plan.cpp", "plan_internal.h"):
-        with open(os.path.join(ROOT, "paper_2410_15332_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        if sources is not None:
+            text = sources[f]
+        else:
+            with open(os.path.join(ROOT, "paper_2410_15332_amd", "csrc", f)) as fh:
+                text = fh.read()
+        h.update(code_without_comments(text).encode())
     return h.hexdigest()[:16]
 
 

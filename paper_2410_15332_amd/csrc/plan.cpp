@@ -346,9 +346,9 @@ void finish_sizes(epic_plan_sizes* s) {
 }
 
 // Attention tiles and split-KV work items of a plan whose S rows and linked
-// tables are written.  Work items are ordered key segment first, so that the
-// workgroups running at the same time read the same KV blocks (one L2 per XCD
-// serves them).
+// tables are written.  Work items go in item_order's launch order (longest key
+// range first; among equal lengths key segment first, so that workgroups that
+// start together read the same KV blocks through their XCD's L2).
 epic_status write_work(const std::vector<Tile>& tiles, int split, const epic_plan_sizes& chk, epic_plan* plan) {
   int part = 0;
   for (size_t t = 0; t < tiles.size(); ++t) {
@@ -359,7 +359,7 @@ epic_status write_work(const std::vector<Tile>& tiles, int split, const epic_pla
     plan->tiles[4 * t + 3] = ns;
     if (ns > 1) part += ns;
   }
-  // work items in launch order (segment-major, longest key range first)
+  // work items in launch order
   int w = 0;
   for (const auto& [t, seg] : item_order(tiles, split)) {
     const int ns = plan->tiles[4 * t + 3];
