@@ -457,3 +457,35 @@ def test_decode_shaped_plans_use_16_row_tiles():
     assert e.value.status == 2
     s = el.epic_plan_sizes_get([el.Request([], [], 40, 0)], el.attn_cfg(32, 8, 128, 0.0, 0, 16), 4)
     assert s.tile_rows == 16 and s.n_tiles == 10        # forced: 4 S rows per tile
+
+
+@pytest.mark.parametrize("lens,suffix,k,split", [
+    ([2048] * 64, 256, 32, 0),     # 256-row tiles, split-KV items of several lengths
+    ([2048] * 64, 256, 4, 0),      # 128-row tiles
+    ([2048] * 24, 256, 32, 256),   # forced split: many equal-length segments
+])
+def test_work_items_longest_first(lens, suffix, k, split):
+    """Launch order: key range (blocks) non-increasing; among equal lengths segment-major
+    (a tile's segment s never precedes a segment s - 1 of equal length of any tile), and
+    every (tile, segment) appears exactly once, covering each tile's blocks."""
+    reqs, n = _long_request(lens, suffix, k)
+    cfg, sizes, v, _ = _plan(reqs, n, 32, 8, split=split)
+    work = v["work"].reshape(-1, 8)[: sizes.n_work]
+    nblk = work[:, 2] - work[:, 1]
+    assert np.all(nblk > 0)
+    assert np.all(np.diff(nblk) <= 0), "work items not longest first"
+    tiles = v["tiles"].reshape(-1, 4)[: sizes.n_tiles]
+    seg = np.zeros(sizes.n_work, np.int64)
+    cover = {}
+    for i, (t, b0, b1) in enumerate(work[:, :3]):
+        p0, ns = int(tiles[t, 2]), int(tiles[t, 3])
+        seg[i] = work[i, 3] - p0 if ns > 1 else 0
+        cover.setdefault(int(t), []).append((int(b0), int(b1)))
+    for L in np.unique(nblk):
+        s = seg[nblk == L]
+        assert np.all(np.diff(s) >= 0), f"segments of length {L} not segment-major"
+    assert len(cover) == sizes.n_tiles
+    for t, ranges in cover.items():
+        ranges.sort()
+        assert all(a[1] == b[0] for a, b in zip(ranges, ranges[1:])), f"tile {t}: segments not contiguous"
+        assert len(ranges) == int(tiles[t, 3])
