@@ -194,13 +194,18 @@ def code_without_comments(text: str) -> str:
     return re.sub(r"\s+", " ", text).strip()
 
 
-def kernel_source_hash(sources=None) -> str:
-    """Hash of what decides an attention launch's memory traffic: the kernel sources
-    and the planner that picks the kernel instance, tiles and split (code only, so an
-    edit of comments keeps a profile valid).  sources: {file name: text} to hash
-    instead of the files in the tree."""
+ATTENTION_SOURCES = ("attention.hip", "device_common.h", "kernels.h", "plan.cpp", "plan_internal.h")
+DECODE_SOURCES = ("decode_attention.hip", "decode_attention.h", "device_common.h", "kernels.h", "plan.cpp",
+                  "plan_internal.h")
+
+
+def kernel_source_hash(sources=None, files=ATTENTION_SOURCES) -> str:
+    """Hash of what decides a kernel launch's memory traffic: the kernel sources and
+    the planner that picks the kernel instance, tiles and split (code only, so an edit
+    of comments keeps a profile valid).  sources: {file name: text} to hash instead of
+    the files in the tree."""
     h = hashlib.sha256()
-    for f in ("attention.hip", "device_common.h", "kernels.h", "plan.cpp", "plan_internal.h"):
+    for f in files:
         if sources is not None:
             text = sources[f]
         else:
@@ -210,18 +215,34 @@ def kernel_source_hash(sources=None) -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(workload: str):
-    """HBM bytes per attention launch from a committed rocprofv3 --pmc summary, if it
-    was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"link_attention_{workload}_traffic.md")
+def traffic_from_profile(workload: str, kernel: str = "link_attention", files=ATTENTION_SOURCES):
+    """HBM bytes per launch of `kernel` from a committed rocprofv3 --pmc summary, if it
+    was taken on the current code; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
     s = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
-    if not m or not s or s.group(1) != kernel_source_hash():
+    if not m or not s or s.group(1) != kernel_source_hash(files=files):
         return None
     return float(m.group(1))
+
+
+def calibration_copy(mib: int):
+    """A plain device-to-device copy of `mib` MiB before the timed region: the known
+    bytes that scale the FETCH_SIZE / WRITE_SIZE counters of a --pmc run."""
+    import torch
+
+    if mib <= 0:
+        return
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    log(f"calibration copy of {mib} MiB done")
 
 
 def cpu_baseline(st, n_rows: int, seed: int = 1):
@@ -593,6 +614,7 @@ def bench_decode(args, wl):
     st.run()
     ds = harness.stage_decode(wl, st.cfg, st.sizes, st.dplan.host, st.spare, st.num_blocks, [1] * wl.batch)
     torch.cuda.synchronize()
+    calibration_copy(args.calibrate_copy_mib)
     for _ in range(args.warmup):
         ds.run(st.k_cache, st.v_cache)
     K = args.steps
@@ -628,7 +650,9 @@ def bench_decode(args, wl):
                      "kernel": (f"link_decode_kernel<{wl.head_dim}>" if ds.sizes.tile_rows == 16
                                 else f"link_attention_kernel<{wl.head_dim}, {ds.sizes.tile_rows // 32}>"),
                      "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                     "algorithmic_bytes_per_launch": kv_bytes, "traffic": None},
+                     "algorithmic_bytes_per_launch": kv_bytes,
+                     "traffic": (traffic_from_profile(args.workload, "link_decode", DECODE_SOURCES)
+                                 if ds.sizes.tile_rows == 16 else None)},
     }
     if not args.no_ttft_medians:
         gms = graph_step_ms(lambda: ds.run(st.k_cache, st.v_cache), K)
@@ -703,14 +727,7 @@ def main():
         f"in {time.time() - t0:.1f}s")
     flops = harness.attention_flops(st.views, wl.num_q_heads, wl.head_dim)
 
-    if args.calibrate_copy_mib > 0:
-        n = args.calibrate_copy_mib * (1 << 20) // 4
-        src = torch.ones(n, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-        log(f"calibration copy of {args.calibrate_copy_mib} MiB done")
+    calibration_copy(args.calibrate_copy_mib)
 
     for _ in range(args.warmup):
         st.run()
