@@ -37,5 +37,6 @@ from .model import (  # noqa: F401
     rmsnorm,
     rope,
     compile_chunk,
+    decoder_layer,
     link_model,
 )

@@ -92,6 +92,20 @@ def _layer(h: np.ndarray, s_pos: np.ndarray, w: Dict[str, np.ndarray], cfg: _Cfg
     return h, k, v
 
 
+def decoder_layer(h: np.ndarray, s_pos: np.ndarray, weights: Dict[str, np.ndarray],
+                  cached_k: Sequence[np.ndarray], cached_v: Sequence[np.ndarray], n_total: int,
+                  hidden: int, ffn: int, hq: int, hkv: int, d: int, theta: float, eps: float,
+                  bf16_storage: bool = True):
+    """One decoder layer of the link step for the selected rows (Sec. 4.2 per-layer
+    recipe inside the Llama block), on its own: h [nS, hidden] is the layer's input
+    hidden rows of S at linked positions s_pos; cached_k / cached_v the layer's chunk
+    caches as compiled.  Returns (h after the layer, recomputed k [nS, Hkv, d], v).
+    This is exactly the step link_model repeats per layer."""
+    cfg = _Cfg(hidden, ffn, hq, hkv, d, theta, eps)
+    return _layer(np.asarray(h, dtype=np.float64), np.asarray(s_pos), weights, cfg, cached_k, cached_v,
+                  n_total, bf16_storage)
+
+
 def link_model(emb_s: np.ndarray, chunk_lens: Sequence[int], suffix_len: int, k: int,
                weights: Sequence[Dict[str, np.ndarray]], final_norm: np.ndarray,
                caches: Sequence[Tuple[Sequence[np.ndarray], Sequence[np.ndarray]]],

@@ -304,14 +304,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     // it owns the tile's first stage (slot 2x + 1), else its first segment (slot 2x).
     // Layout: [wavefront][tile t][register quad][lane][4] floats, so each access is
     // 16 bytes per lane, 1 KB per instruction.  Partials are written and read with
-    // device-coherent accesses (sc1), which go past the XCD's L2, so no cache-wide
-    // write-back or invalidate is needed.
+    // agent-scope accesses (cache policy sc1 = device scope on gfx950), which go past
+    // the XCD's L2, so no cache-wide write-back or invalidate is needed.
     const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
         g.partial, 0, 2 * kMaxWorkers * kPartialFloats * 4, kBufWord3);
     auto slot_off = [&](int x) __attribute__((always_inline)) {   // bytes
       return int((2 * x + (x == wf ? 1 : 0)) * kPartialFloats + wv * kWaveFloats) * 4 + lane * 16;
     };
-    constexpr int kSc1 = 16;             // cache policy: system coherent
+    constexpr int kSc1 = 16;             // cache policy sc1 alone: agent (device) scope
     typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
     const int mine = slot_off(wr);
 #pragma unroll
@@ -326,10 +326,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     // Each wavefront keeps its own arrival counter for the tile (its part of the
     // tile depends only on the same wavefront's part of the other partials), so no
     // workgroup barrier is needed: the last wavefront to arrive finishes that part.
+    // The counter bump is an agent-scope atomic.  The hardware wait orders it after this
+    // wavefront's partial stores; the compiler-only fences on both sides keep the
+    // compiler from moving the stores below it or the partial loads above it (they
+    // emit no instruction, so no L2 write-back).
     wait_vmem<0>();                      // this wavefront's partial has landed
     int* cnt = g.tile_count + q * (kThreads / 64) + wv;
     int before = 0;
-    if (lane == 0) before = atomicAdd(cnt, 1);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    if (lane == 0) before = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
     before = __builtin_amdgcn_readfirstlane(before);
     if (before != wl - wf) return;       // not the last to arrive
 #pragma unroll
@@ -351,7 +357,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
       }
       epilogue_part(mt, nt, h, v);
     }
-    if (lane == 0) atomicExch(cnt, 0);   // ready for the next launch
+    if (lane == 0) __hip_atomic_exchange(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);   // ready for the next launch
   };
 
   // ---- pipeline: unit u (one K stage of one tile) lives in LDS buffer u % NS.

@@ -91,9 +91,13 @@ def dummy_embeddings(seed: int, n_dummy: int, hidden: int) -> np.ndarray:
 W_ATTN_NORM, W_QKV, W_O, W_MLP_NORM, W_GATE_UP, W_DOWN, W_FINAL_NORM = range(7)
 
 
-def _weight(seed: int, layer: int, tid: int, shape, fan_in: int) -> np.ndarray:
-    rng = np.random.default_rng([seed, _W, layer, tid])
-    return _normal_bf16(rng, shape, 0.5 / np.sqrt(fan_in))
+_SLAB_ROWS = 512      # linear weights are drawn in slabs of this many rows, one stream each
+
+
+def _weight_slab(seed: int, layer: int, tid: int, shape, fan_in: int, slab: int) -> np.ndarray:
+    rng = np.random.default_rng([seed, _W, layer, tid, slab])
+    rows = min(_SLAB_ROWS, shape[0] - slab * _SLAB_ROWS)
+    return _normal_bf16(rng, (rows, shape[1]), 0.5 / np.sqrt(fan_in))
 
 
 def _norm_weight(seed: int, layer: int, tid: int, n: int) -> np.ndarray:
@@ -107,21 +111,32 @@ def model_weights(seed: int, layer: int, hidden: int, ffn: int, hq: int, hkv: in
     """bf16-bit weights of one decoder layer in [out, in] layout.
 
     wqkv rows: [Hq*d query | Hkv*d key | Hkv*d value]; w_gate_up rows: [ffn gate | ffn up].
-    Linear weights are N(0, (0.5/sqrt(fan_in))^2); norm weights 1 + 0.1*N(0, 1).
+    Linear weights are N(0, (0.5/sqrt(fan_in))^2), drawn in slabs of 512 rows with one
+    random stream per slab (so they can be drawn in parallel); norm weights 1 + 0.1*N(0, 1).
     """
-    jobs = {
-        "attn_norm": lambda: _norm_weight(seed, layer, W_ATTN_NORM, hidden),
-        "wqkv": lambda: _weight(seed, layer, W_QKV, ((hq + 2 * hkv) * d, hidden), hidden),
-        "wo": lambda: _weight(seed, layer, W_O, (hidden, hq * d), hq * d),
-        "mlp_norm": lambda: _norm_weight(seed, layer, W_MLP_NORM, hidden),
-        "w_gate_up": lambda: _weight(seed, layer, W_GATE_UP, (2 * ffn, hidden), hidden),
-        "w_down": lambda: _weight(seed, layer, W_DOWN, (hidden, ffn), ffn),
-    }
+    linear = {"wqkv": (W_QKV, ((hq + 2 * hkv) * d, hidden), hidden),
+              "wo": (W_O, (hidden, hq * d), hq * d),
+              "w_gate_up": (W_GATE_UP, (2 * ffn, hidden), hidden),
+              "w_down": (W_DOWN, (hidden, ffn), ffn)}
+    out = {"attn_norm": _norm_weight(seed, layer, W_ATTN_NORM, hidden),
+           "mlp_norm": _norm_weight(seed, layer, W_MLP_NORM, hidden)}
+    for name, (_, shape, _) in linear.items():
+        out[name] = np.empty(shape, np.uint16)
+    jobs = [(name, slab) for name, (_, shape, _) in linear.items()
+            for slab in range(-(-shape[0] // _SLAB_ROWS))]
+
+    def fill(job):
+        name, slab = job
+        tid, shape, fan_in = linear[name]
+        out[name][slab * _SLAB_ROWS:(slab + 1) * _SLAB_ROWS] = _weight_slab(seed, layer, tid, shape, fan_in, slab)
+
     if threads <= 1:
-        return {k: f() for k, f in jobs.items()}
-    with ThreadPoolExecutor(threads) as ex:
-        futs = {k: ex.submit(f) for k, f in jobs.items()}
-        return {k: f.result() for k, f in futs.items()}
+        for job in jobs:
+            fill(job)
+    else:
+        with ThreadPoolExecutor(threads) as ex:
+            list(ex.map(fill, jobs))
+    return {k: out[k] for k in ("attn_norm", "wqkv", "wo", "mlp_norm", "w_gate_up", "w_down")}
 
 
 def final_norm_weight(seed: int, hidden: int) -> np.ndarray:

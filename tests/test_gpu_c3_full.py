@@ -1,0 +1,245 @@
+"""GPU parity of the 32-layer Llama-3-8B-shaped link step at its stated size.
+
+Workload: hidden 4096, FFN 14336 (SwiGLU), GQA 32/8, head dim 128, rotary base
+5e5, 20 chunks x 1024 tokens compiled on the GPU at positions 0..1023
+(epic_plan_compile + epic_link_model), LegoLink-32 plus 128 suffix tokens: 736
+selected rows through all 32 layers.  Weights are seeded synth draws shared
+with the oracle.
+
+The float64 oracle cannot afford the compile of all 20 chunks (about 290 TFLOP),
+so, as Sec. 4.2's recipe is per layer, the checks are:
+  * compile parity at full width: chunk 0 compiled by the oracle (all 32 layers,
+    1024 rows) against the GPU's chunk-0 cache of every layer and its compiled
+    hidden rows;
+  * teacher-forced link parity per layer: epic_link_layer runs one layer at a
+    time; the oracle's decoder_layer gets the GPU's input hidden rows of that
+    layer and the GPU-compiled chunk caches, and its output hidden rows and
+    recomputed K/V (bf16) are compared with the GPU's;
+  * end-to-end link parity: epic_link_model over all layers against the
+    oracle's layer chain from the same embeddings (its caches again the
+    GPU-compiled ones), final hidden after the last RMSNorm and every layer's
+    recomputed K/V.
+Bar everywhere: max |err| <= 2e-2 (bf16 K/V; fp32 hidden rows of magnitude ~1).
+
+The oracle work (about 100 layer evaluations) runs on a background thread pool
+started by the module fixture; each test waits for its part, so results come
+in as the chains advance.
+"""
+import threading
+import time
+from concurrent.futures import Future, ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+import synth  # noqa: E402
+from synth.configs import get_config  # noqa: E402
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
+
+ATOL = 2e-2
+N_LAYERS = 32
+GROUPS = [range(i, i + 8) for i in range(0, N_LAYERS, 8)]
+
+
+def _f64(bits):
+    return synth.bf16_bits_to_f32(bits).astype(np.float64)
+
+
+def _bits(t):
+    return t.detach().cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+def _log(msg):
+    print(f"[gpu-test c3] {msg}", flush=True)
+
+
+class _C3:
+    """GPU results of the staged workload and the oracle chains computing against them."""
+
+    def __init__(self):
+        from paper_2410_15332_amd import epic_link as el
+        from paper_2410_15332_amd import harness
+
+        t0 = time.time()
+        wl = get_config("c3")
+        assert wl.n_layers == N_LAYERS
+        self.wl = wl
+        self.dims = dict(hidden=wl.hidden, ffn=wl.ffn, hq=wl.num_q_heads, hkv=wl.num_kv_heads, d=wl.head_dim,
+                         theta=wl.rope_theta, eps=wl.rms_eps)
+        self.weights = [synth.model_weights(wl.seed, l, wl.hidden, wl.ffn, wl.num_q_heads, wl.num_kv_heads,
+                                            wl.head_dim, threads=16) for l in range(N_LAYERS)]
+        self.final_norm = synth.final_norm_weight(wl.seed, wl.hidden)
+        dev = [{k: harness._bf16_tensor(v, "cuda") for k, v in w.items()} for w in self.weights]
+        _log(f"weights drawn and uploaded in {time.time() - t0:.1f}s")
+        st = harness.stage_model(wl, caches="compile", keep_compile=True, weights=dev)
+        torch.cuda.synchronize()
+        self.st = st
+        self.s_pos = st.views["s_pos"].astype(np.int64)
+        self.n_total = wl.linked_len
+        _log(f"staged (GPU compile of 20 x 1024 rows done), n_s={st.sizes.n_s}, {time.time() - t0:.1f}s")
+
+        # the compile's chunk-0 hidden rows, and every layer's chunk caches (token-major bf16 bits)
+        cst = st.compile_stage
+        a = int(cst.views["s_off"][0])
+        self.compiled_hidden0 = cst.out[a:a + wl.chunk_lens[0]].double().cpu().numpy()
+        st.compile_stage = None
+        del cst
+        hkv, d = wl.num_kv_heads, wl.head_dim
+        self.chunk_kv = []
+        for layer in range(N_LAYERS):
+            kc, vc = _bits(st.k_caches[layer]), _bits(st.v_caches[layer])
+            ks, vs = [], []
+            for j, blocks in enumerate(st.chunk_block_ids):
+                L = wl.chunk_lens[j]
+                ks.append(kc[blocks].transpose(0, 2, 1, 3).reshape(-1, hkv, d)[:L].copy())
+                vs.append(vc[blocks].transpose(0, 3, 1, 2).reshape(-1, hkv, d)[:L].copy())
+            self.chunk_kv.append((ks, vs))
+
+        # end to end: epic_link_model, all layers
+        st.run()
+        torch.cuda.synchronize()
+        self.e2e_out = st.out.double().cpu().numpy()
+        self.e2e_kv = [self._s_rows(layer) for layer in range(N_LAYERS)]
+
+        # teacher-forced: epic_link_layer one layer at a time, inputs and outputs kept
+        hidden = st.hidden
+        hidden.copy_(st.emb)
+        self.tf_in, self.tf_out, self.tf_kv = [], [], []
+        for layer in range(N_LAYERS):
+            self.tf_in.append(hidden.double().cpu().numpy())
+            el.epic_link_layer(st.cfg, st.layers[layer], st.dplan, hidden, st.k_caches[layer],
+                               st.v_caches[layer], st.workspace)
+            torch.cuda.synchronize()
+            self.tf_out.append(hidden.double().cpu().numpy())
+            self.tf_kv.append(self._s_rows(layer))
+        _log(f"GPU runs done in {time.time() - t0:.1f}s; starting the oracle chains")
+
+        self.emb = st.emb.double().cpu().numpy()
+        self.stop = threading.Event()
+        self.pool = ThreadPoolExecutor(8)
+        self.e2e_ref = [Future() for _ in range(N_LAYERS + 1)]
+        threading.Thread(target=self._e2e_chain, daemon=True).start()
+        # the two sequential chains (end to end, compile) first, then the independent layers
+        self.compile_ref = self.pool.submit(self._compile_chunk0)
+        self.tf_ref = [self.pool.submit(self._tf_layer, layer) for layer in range(N_LAYERS)]
+
+    def _s_rows(self, layer):
+        from paper_2410_15332_amd import epic_link as el
+        K, V = el.read_linked_kv(_bits(self.st.k_caches[layer]), _bits(self.st.v_caches[layer]), self.st.views, 0)
+        return K[self.s_pos].copy(), V[self.s_pos].copy()
+
+    def caches(self, layer):
+        ks, vs = self.chunk_kv[layer]
+        return [_f64(k) for k in ks], [_f64(v) for v in vs]
+
+    def _tf_layer(self, layer):
+        if self.stop.is_set():
+            return None
+        ck, cv = self.caches(layer)
+        return oracle.decoder_layer(self.tf_in[layer], self.s_pos, self.weights[layer], ck, cv, self.n_total,
+                                    **self.dims)
+
+    def _compile_chunk0(self):
+        wl = self.wl
+        emb = synth.token_embeddings(wl.seed, 0, 0, range(wl.chunk_lens[0]), wl.hidden).astype(np.float64)
+        return oracle.compile_chunk(emb, self.weights, self.final_norm, **self.dims)
+
+    def _e2e_chain(self):
+        """The oracle's link step layer after layer (what oracle.link_model does), from the
+        same embeddings, each layer's result published as soon as it is ready."""
+        h = self.emb
+        try:
+            for layer in range(N_LAYERS):
+                if self.stop.is_set():
+                    raise RuntimeError("stopped")
+                ck, cv = self.caches(layer)
+                h, k, v = oracle.decoder_layer(h, self.s_pos, self.weights[layer], ck, cv, self.n_total,
+                                               **self.dims)
+                self.e2e_ref[layer].set_result((k, v))
+            self.e2e_ref[N_LAYERS].set_result(oracle.rmsnorm(h, _f64(self.final_norm), self.wl.rms_eps))
+        except BaseException as e:  # noqa: BLE001 -- handed to the waiting tests
+            for f in self.e2e_ref:
+                if not f.done():
+                    f.set_exception(e)
+
+    def close(self):
+        self.stop.set()
+        self.pool.shutdown(wait=False, cancel_futures=True)
+
+
+@pytest.fixture(scope="module")
+def c3():
+    run = _C3()
+    yield run
+    run.close()
+
+
+def test_c3_selection(c3):
+    wl = c3.wl
+    ref = oracle.legolink_positions(wl.chunk_lens, wl.suffix_len, wl.k)
+    assert np.array_equal(c3.s_pos, ref), "planner selection differs from the oracle"
+    assert len(ref) == 19 * 32 + 128
+
+
+@pytest.mark.parametrize("group", range(len(GROUPS)), ids=[f"layers{g[0]}-{g[-1]}" for g in GROUPS])
+def test_c3_teacher_forced(c3, group):
+    """Layer by layer, each fed the GPU's own input rows of that layer."""
+    worst = [0.0, 0.0]
+    for layer in GROUPS[group]:
+        h_ref, k_ref, v_ref = c3.tf_ref[layer].result()
+        eh = np.abs(c3.tf_out[layer] - h_ref).max()
+        gk, gv = c3.tf_kv[layer]
+        ekv = max(np.abs(_f64(gk) - k_ref).max(), np.abs(_f64(gv) - v_ref).max())
+        _log(f"teacher-forced layer {layer}: hidden max|err| {eh:.3e} (rms {np.sqrt(np.mean(h_ref ** 2)):.2f}), "
+             f"recomputed K/V max|err| {ekv:.3e}")
+        assert eh <= ATOL, f"layer {layer}: output hidden max |err| {eh}"
+        assert ekv <= ATOL, f"layer {layer}: recomputed K/V max |err| {ekv}"
+        worst = [max(worst[0], eh), max(worst[1], ekv)]
+    _log(f"teacher-forced layers {GROUPS[group][0]}-{GROUPS[group][-1]}: worst hidden {worst[0]:.3e}, "
+         f"K/V {worst[1]:.3e}")
+
+
+def test_c3_teacher_forced_chain_is_the_model_step(c3):
+    """epic_link_layer 32 times and epic_link_model run the same kernels on the same
+    inputs: the recomputed K/V of every layer agree bit for bit."""
+    for layer in range(N_LAYERS):
+        assert np.array_equal(c3.tf_kv[layer][0], c3.e2e_kv[layer][0]), f"layer {layer}: K"
+        assert np.array_equal(c3.tf_kv[layer][1], c3.e2e_kv[layer][1]), f"layer {layer}: V"
+
+
+def test_c3_compile_chunk_full_width(c3):
+    """Compile step at full width: chunk 0 (1024 tokens, positions 0..1023) through all
+    32 layers by the oracle against the GPU compile's chunk-0 cache and hidden rows."""
+    out_ref, kv_ref = c3.compile_ref.result()
+    worst = 0.0
+    for layer, (k_ref, v_ref) in enumerate(kv_ref):
+        ks, vs = c3.chunk_kv[layer]
+        e = max(np.abs(_f64(ks[0]) - k_ref).max(), np.abs(_f64(vs[0]) - v_ref).max())
+        assert e <= ATOL, f"layer {layer}: compiled chunk-0 K/V max |err| {e}"
+        worst = max(worst, e)
+    eh = np.abs(c3.compiled_hidden0 - out_ref).max()
+    _log(f"compile chunk 0 (1024 rows, 32 layers): K/V max|err| {worst:.3e}, final hidden max|err| {eh:.3e}")
+    assert eh <= ATOL, f"compiled hidden max |err| {eh}"
+
+
+@pytest.mark.parametrize("group", range(len(GROUPS)), ids=[f"layers{g[0]}-{g[-1]}" for g in GROUPS])
+def test_c3_end_to_end(c3, group):
+    """epic_link_model against the oracle's chain from the same embeddings: recomputed
+    K/V of every layer, and (last group) the final hidden rows after the last RMSNorm."""
+    worst = 0.0
+    for layer in GROUPS[group]:
+        k_ref, v_ref = c3.e2e_ref[layer].result()
+        gk, gv = c3.e2e_kv[layer]
+        e = max(np.abs(_f64(gk) - k_ref).max(), np.abs(_f64(gv) - v_ref).max())
+        _log(f"end to end layer {layer}: recomputed K/V max|err| {e:.3e}")
+        assert e <= ATOL, f"layer {layer}: recomputed K/V max |err| {e}"
+        worst = max(worst, e)
+    if GROUPS[group][-1] == N_LAYERS - 1:
+        out_ref = c3.e2e_ref[N_LAYERS].result()
+        err = np.abs(c3.e2e_out - out_ref)
+        _log(f"end to end final hidden: max|err| {err.max():.3e}, mean {err.mean():.2e}")
+        assert err.max() <= ATOL, f"final hidden max |err| {err.max()}"

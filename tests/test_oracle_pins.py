@@ -332,6 +332,46 @@ def test_bf16_storage_stays_close():
     assert np.abs(o64 - o16).max() < 5e-2
 
 
+def test_round_bf16_matches_library_cast():
+    """The oracle's bf16 storage rounding (float64 -> float32 -> bf16, nearest, ties to
+    even) against torch's float32 -> bfloat16 conversion: random values over many
+    binades, exact ties with even and odd kept halves, near ties either side,
+    carries into the next binade, signed zeros, subnormals and overflow to inf."""
+    from oracle.link import _round_bf16
+    rng = np.random.default_rng(11)
+    vals = [rng.standard_normal(200000) * np.exp2(rng.integers(-30, 30, 200000))]
+    hi = rng.integers(0, 1 << 16, 50000, dtype=np.uint32) << np.uint32(16)
+    for low in (0x8000, 0x7FFF, 0x8001, 0x0001, 0xFFFF, 0x0000):     # ties, near ties, extremes
+        f = (hi | np.uint32(low)).view(np.float32)
+        vals.append(f[np.isfinite(f)].astype(np.float64))          # NaN patterns are not a rounding question
+    vals.append(np.array([0.0, -0.0, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, -(1.0 + 2.0 ** -8),
+                          np.float32(np.finfo(np.float32).max), 2.0 ** -140, 2.0 ** -149, 3.0 * 2.0 ** -134]))
+    x = np.concatenate(vals)
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    got = _round_bf16(x)
+    assert np.array_equal(np.signbit(got), np.signbit(ref))
+    assert np.array_equal(got, ref)
+    # hand-worked cases (bf16 keeps 8 significant bits: the spacing at 1 is 2^-7)
+    r = _round_bf16(np.array([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, 1.0 + 2.0 ** -8 + 2.0 ** -20, -1.5 - 2.0 ** -9]))
+    assert r.tolist() == [1.0, 1.0 + 2.0 ** -6, 1.0 + 2.0 ** -7, -1.5]
+
+
+def test_masked_attention_row_subset_equals_full():
+    """Computing some rows of S (any order of groups, any group size) gives those rows
+    of the full result: rows are independent, so sampled parity checks are sound."""
+    rng = np.random.default_rng(12)
+    n_total, hkv, hq, d = 300, 2, 4, 16
+    K = rng.standard_normal((n_total, hkv, d))
+    V = rng.standard_normal((n_total, hkv, d))
+    s_pos = np.sort(rng.choice(n_total, 57, replace=False))
+    q = rng.standard_normal((57, hq, d))
+    out, lse = oracle.masked_attention(q, K, V, s_pos)
+    for rows, group in (([0, 56], 256), (rng.choice(57, 20, replace=False), 3), (np.arange(57), 7)):
+        o2, l2 = oracle.masked_attention(q, K, V, s_pos, rows=rows, row_group=group)
+        np.testing.assert_allclose(o2, out[rows], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(l2, lse[rows], rtol=0, atol=1e-12)
+
+
 def test_rope_properties():
     rng = np.random.default_rng(2)
     x = rng.standard_normal((5, 3, 16))
