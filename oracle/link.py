@@ -123,7 +123,11 @@ def masked_attention(q: np.ndarray, K_exp: np.ndarray, V_exp: np.ndarray, s_pos:
 
     ``rows`` restricts the computation to some rows of S (each row is
     independent); rows are processed ``row_group`` at a time to bound memory.
+    The steps run as float64 PyTorch CPU operations (multi-threaded library
+    matmul, exp and sums; nothing fused or reordered).
     """
+    import torch
+
     n_s, hq, d = q.shape
     hkv = K_exp.shape[1]
     G = hq // hkv
@@ -132,21 +136,25 @@ def masked_attention(q: np.ndarray, K_exp: np.ndarray, V_exp: np.ndarray, s_pos:
     rows = np.arange(n_s) if rows is None else np.asarray(rows, dtype=np.int64)
     out = np.zeros((len(rows), hq, d))
     lse = np.zeros((len(rows), hq))
+    qt = torch.from_numpy(np.ascontiguousarray(q, dtype=np.float64))
+    n_max = int(np.asarray(s_pos)[rows].max()) + 1 if len(rows) else 0
+    Kg = [torch.from_numpy(np.ascontiguousarray(K_exp[:n_max, g, :], dtype=np.float64)) for g in range(hkv)]
+    Vg = [torch.from_numpy(np.ascontiguousarray(V_exp[:n_max, g, :], dtype=np.float64)) for g in range(hkv)]
     for g0 in range(0, len(rows), row_group):
         rr = rows[g0:g0 + row_group]
-        p = s_pos[rr]
+        p = torch.from_numpy(np.asarray(s_pos)[rr].astype(np.int64))
         n_keys = int(p.max()) + 1
-        key_pos = np.arange(n_keys)
-        masked = key_pos[None, :] > p[:, None]          # key after the query: excluded
+        masked = torch.arange(n_keys)[None, :] > p[:, None]    # key after the query: excluded
+        rt = torch.from_numpy(rr)
         for h in range(hq):
             g = h // G
-            logits = scale * (q[rr, h, :].astype(np.float64) @ K_exp[:n_keys, g, :].T)
-            logits[masked] = -np.inf
-            m = logits.max(axis=1, keepdims=True)
-            e = np.exp(logits - m)
-            denom = e.sum(axis=1, keepdims=True)
-            out[g0:g0 + len(rr), h, :] = (e @ V_exp[:n_keys, g, :]) / denom
-            lse[g0:g0 + len(rr), h] = (m + np.log(denom))[:, 0]
+            logits = scale * (qt[rt, h, :] @ Kg[g][:n_keys].T)
+            logits.masked_fill_(masked, -np.inf)
+            m = logits.amax(dim=1, keepdim=True)
+            e = torch.exp(logits - m)
+            denom = e.sum(dim=1, keepdim=True)
+            out[g0:g0 + len(rr), h, :] = ((e @ Vg[g][:n_keys]) / denom).numpy()
+            lse[g0:g0 + len(rr), h] = (m + torch.log(denom))[:, 0].numpy()
     return out, lse
 
 

@@ -30,8 +30,11 @@ from .link import _round_bf16, expand_kv, legolink_positions, masked_attention, 
 
 
 def _bf16_to_f64(bits: np.ndarray) -> np.ndarray:
-    u = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
-    return u.view(np.float32).astype(np.float64)
+    """Exact widening of bf16 bit patterns to float64 (a multi-threaded library cast)."""
+    import torch
+
+    b = np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16)
+    return torch.from_numpy(b).view(torch.bfloat16).to(torch.float64).numpy()
 
 
 def rmsnorm(x: np.ndarray, w: np.ndarray, eps: float) -> np.ndarray:

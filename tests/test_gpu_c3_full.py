@@ -21,13 +21,13 @@ so, as Sec. 4.2's recipe is per layer, the checks are:
     recomputed K/V.
 Bar everywhere: max |err| <= 2e-2 (bf16 K/V; fp32 hidden rows of magnitude ~1).
 
-The oracle work (about 100 layer evaluations) runs on a background thread pool
-started by the module fixture; each test waits for its part, so results come
-in as the chains advance.
+The oracle work (about 100 layer evaluations) runs on one background thread
+started by the module fixture, in the order the tests consume it; each test
+waits for its part.
 """
 import threading
 import time
-from concurrent.futures import Future, ThreadPoolExecutor
+from concurrent.futures import Future
 
 import numpy as np
 import pytest
@@ -120,12 +120,19 @@ class _C3:
 
         self.emb = st.emb.double().cpu().numpy()
         self.stop = threading.Event()
-        self.pool = ThreadPoolExecutor(8)
-        self.e2e_ref = [Future() for _ in range(N_LAYERS + 1)]
-        threading.Thread(target=self._e2e_chain, daemon=True).start()
-        # the two sequential chains (end to end, compile) first, then the independent layers
-        self.compile_ref = self.pool.submit(self._compile_chunk0)
-        self.tf_ref = [self.pool.submit(self._tf_layer, layer) for layer in range(N_LAYERS)]
+        # one background thread runs the oracle work in the order the tests consume it
+        # (each step uses every core through the library calls inside it): per group of
+        # 8 layers the teacher-forced layers, then the end-to-end chain through them;
+        # the compile of chunk 0 last
+        self.ref = {}
+        for g in GROUPS:
+            for layer in g:
+                self.ref[("tf", layer)] = Future()
+            for layer in g:
+                self.ref[("e2e", layer)] = Future()
+        self.ref["e2e_final"] = Future()
+        self.ref["compile"] = Future()
+        threading.Thread(target=self._oracle_worker, daemon=True).start()
 
     def _s_rows(self, layer):
         from paper_2410_15332_amd import epic_link as el
@@ -136,39 +143,39 @@ class _C3:
         ks, vs = self.chunk_kv[layer]
         return [_f64(k) for k in ks], [_f64(v) for v in vs]
 
-    def _tf_layer(self, layer):
-        if self.stop.is_set():
-            return None
-        ck, cv = self.caches(layer)
-        return oracle.decoder_layer(self.tf_in[layer], self.s_pos, self.weights[layer], ck, cv, self.n_total,
-                                    **self.dims)
-
-    def _compile_chunk0(self):
+    def _oracle_worker(self):
         wl = self.wl
-        emb = synth.token_embeddings(wl.seed, 0, 0, range(wl.chunk_lens[0]), wl.hidden).astype(np.float64)
-        return oracle.compile_chunk(emb, self.weights, self.final_norm, **self.dims)
-
-    def _e2e_chain(self):
-        """The oracle's link step layer after layer (what oracle.link_model does), from the
-        same embeddings, each layer's result published as soon as it is ready."""
-        h = self.emb
+        h = self.emb                      # the end-to-end chain's hidden rows
+        t0 = time.time()
         try:
-            for layer in range(N_LAYERS):
+            for key, fut in self.ref.items():
                 if self.stop.is_set():
                     raise RuntimeError("stopped")
-                ck, cv = self.caches(layer)
-                h, k, v = oracle.decoder_layer(h, self.s_pos, self.weights[layer], ck, cv, self.n_total,
+                if key == "e2e_final":
+                    # the oracle's link step ends with the final RMSNorm (as oracle.link_model)
+                    fut.set_result(oracle.rmsnorm(h, _f64(self.final_norm), wl.rms_eps))
+                elif key == "compile":
+                    emb = synth.token_embeddings(wl.seed, 0, 0, range(wl.chunk_lens[0]), wl.hidden)
+                    fut.set_result(oracle.compile_chunk(emb.astype(np.float64), self.weights, self.final_norm,
+                                                        **self.dims))
+                else:
+                    kind, layer = key
+                    ck, cv = self.caches(layer)
+                    h_in = self.tf_in[layer] if kind == "tf" else h
+                    res = oracle.decoder_layer(h_in, self.s_pos, self.weights[layer], ck, cv, self.n_total,
                                                **self.dims)
-                self.e2e_ref[layer].set_result((k, v))
-            self.e2e_ref[N_LAYERS].set_result(oracle.rmsnorm(h, _f64(self.final_norm), self.wl.rms_eps))
+                    if kind == "e2e":
+                        h = res[0]
+                        res = res[1:]
+                    fut.set_result(res)
+                print(f"[gpu-test c3] oracle {key} done at {time.time() - t0:.1f}s", flush=True)
         except BaseException as e:  # noqa: BLE001 -- handed to the waiting tests
-            for f in self.e2e_ref:
+            for f in self.ref.values():
                 if not f.done():
                     f.set_exception(e)
 
     def close(self):
         self.stop.set()
-        self.pool.shutdown(wait=False, cancel_futures=True)
 
 
 @pytest.fixture(scope="module")
@@ -186,11 +193,14 @@ def test_c3_selection(c3):
 
 
 @pytest.mark.parametrize("group", range(len(GROUPS)), ids=[f"layers{g[0]}-{g[-1]}" for g in GROUPS])
-def test_c3_teacher_forced(c3, group):
-    """Layer by layer, each fed the GPU's own input rows of that layer."""
-    worst = [0.0, 0.0]
+def test_c3_link_layers(c3, group):
+    """Per layer of the group: teacher-forced (each layer fed the GPU's own input rows of
+    that layer: output hidden rows and recomputed K/V), then end to end (epic_link_model
+    against the oracle's chain from the same embeddings: recomputed K/V of every layer,
+    and after the last layer the final hidden rows after the last RMSNorm)."""
+    worst = [0.0, 0.0, 0.0]
     for layer in GROUPS[group]:
-        h_ref, k_ref, v_ref = c3.tf_ref[layer].result()
+        h_ref, k_ref, v_ref = c3.ref[("tf", layer)].result()
         eh = np.abs(c3.tf_out[layer] - h_ref).max()
         gk, gv = c3.tf_kv[layer]
         ekv = max(np.abs(_f64(gk) - k_ref).max(), np.abs(_f64(gv) - v_ref).max())
@@ -198,9 +208,21 @@ def test_c3_teacher_forced(c3, group):
              f"recomputed K/V max|err| {ekv:.3e}")
         assert eh <= ATOL, f"layer {layer}: output hidden max |err| {eh}"
         assert ekv <= ATOL, f"layer {layer}: recomputed K/V max |err| {ekv}"
-        worst = [max(worst[0], eh), max(worst[1], ekv)]
-    _log(f"teacher-forced layers {GROUPS[group][0]}-{GROUPS[group][-1]}: worst hidden {worst[0]:.3e}, "
-         f"K/V {worst[1]:.3e}")
+        worst[0], worst[1] = max(worst[0], eh), max(worst[1], ekv)
+    for layer in GROUPS[group]:
+        k_ref, v_ref = c3.ref[("e2e", layer)].result()
+        gk, gv = c3.e2e_kv[layer]
+        e = max(np.abs(_f64(gk) - k_ref).max(), np.abs(_f64(gv) - v_ref).max())
+        _log(f"end to end layer {layer}: recomputed K/V max|err| {e:.3e}")
+        assert e <= ATOL, f"layer {layer}: end-to-end recomputed K/V max |err| {e}"
+        worst[2] = max(worst[2], e)
+    _log(f"layers {GROUPS[group][0]}-{GROUPS[group][-1]}: teacher-forced worst hidden {worst[0]:.3e}, "
+         f"K/V {worst[1]:.3e}; end-to-end K/V {worst[2]:.3e}")
+    if GROUPS[group][-1] == N_LAYERS - 1:
+        out_ref = c3.ref["e2e_final"].result()
+        err = np.abs(c3.e2e_out - out_ref)
+        _log(f"end to end final hidden: max|err| {err.max():.3e}, mean {err.mean():.2e}")
+        assert err.max() <= ATOL, f"final hidden max |err| {err.max()}"
 
 
 def test_c3_teacher_forced_chain_is_the_model_step(c3):
@@ -214,7 +236,7 @@ def test_c3_teacher_forced_chain_is_the_model_step(c3):
 def test_c3_compile_chunk_full_width(c3):
     """Compile step at full width: chunk 0 (1024 tokens, positions 0..1023) through all
     32 layers by the oracle against the GPU compile's chunk-0 cache and hidden rows."""
-    out_ref, kv_ref = c3.compile_ref.result()
+    out_ref, kv_ref = c3.ref["compile"].result()
     worst = 0.0
     for layer, (k_ref, v_ref) in enumerate(kv_ref):
         ks, vs = c3.chunk_kv[layer]
@@ -224,22 +246,3 @@ def test_c3_compile_chunk_full_width(c3):
     eh = np.abs(c3.compiled_hidden0 - out_ref).max()
     _log(f"compile chunk 0 (1024 rows, 32 layers): K/V max|err| {worst:.3e}, final hidden max|err| {eh:.3e}")
     assert eh <= ATOL, f"compiled hidden max |err| {eh}"
-
-
-@pytest.mark.parametrize("group", range(len(GROUPS)), ids=[f"layers{g[0]}-{g[-1]}" for g in GROUPS])
-def test_c3_end_to_end(c3, group):
-    """epic_link_model against the oracle's chain from the same embeddings: recomputed
-    K/V of every layer, and (last group) the final hidden rows after the last RMSNorm."""
-    worst = 0.0
-    for layer in GROUPS[group]:
-        k_ref, v_ref = c3.e2e_ref[layer].result()
-        gk, gv = c3.e2e_kv[layer]
-        e = max(np.abs(_f64(gk) - k_ref).max(), np.abs(_f64(gv) - v_ref).max())
-        _log(f"end to end layer {layer}: recomputed K/V max|err| {e:.3e}")
-        assert e <= ATOL, f"layer {layer}: recomputed K/V max |err| {e}"
-        worst = max(worst, e)
-    if GROUPS[group][-1] == N_LAYERS - 1:
-        out_ref = c3.e2e_ref[N_LAYERS].result()
-        err = np.abs(c3.e2e_out - out_ref)
-        _log(f"end to end final hidden: max|err| {err.max():.3e}, mean {err.mean():.2e}")
-        assert err.max() <= ATOL, f"final hidden max |err| {err.max()}"
