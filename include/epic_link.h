@@ -27,7 +27,8 @@
  *    and return without synchronising.  Argument errors are detected on the host
  *    before anything is enqueued; nothing is launched when a call fails.
  *  - No entry point allocates device memory; scratch space is the caller's
- *    `workspace` of at least the size the matching *_workspace_bytes call returns.
+ *    `workspace` of at least the size the matching *_workspace_bytes call returns
+ *    (epic_link_attention_noalloc instead uses a fixed device array of the library).
  *  - Return value: EPIC_OK or an error code; epic_last_error() gives detail
  *    (thread-local, valid until the next call on the same thread).
  */
@@ -248,6 +249,26 @@ epic_status epic_link_attention(const epic_attn_cfg* cfg, const epic_plan_sizes*
                                 uint16_t* k_cache, uint16_t* v_cache,
                                 uint16_t* out, float* lse,
                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* epic_link_attention for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * steps, kernels and results, with the split-KV partials kept in a fixed array of
+ * EPIC_NOALLOC_SCRATCH_BYTES of device memory that the library holds, one copy per
+ * GPU, from the time its code is loaded on that GPU until the process ends.  The
+ * caller still passes inputs, caches and outputs (as for epic_link_attention); no
+ * device memory is allocated or freed by the call.  A plan whose partials need more
+ * than EPIC_NOALLOC_SCRATCH_BYTES (epic_link_workspace_bytes) is rejected with
+ * EPIC_ERR_WORKSPACE before anything is enqueued (a larger kv_split_blocks gives fewer
+ * partials).  Every call on one GPU shares that GPU's array: calls whose work overlaps
+ * in time on one GPU (other streams, other threads) race and give wrong results;
+ * calls in one stream are ordered and safe.  Nothing in the array needs to start at
+ * any value: each call writes every partial it reads. */
+#define EPIC_NOALLOC_SCRATCH_BYTES (96u << 20)
+epic_status epic_link_attention_noalloc(const epic_attn_cfg* cfg, const epic_plan_sizes* sizes,
+                                        const epic_plan* plan_dev,
+                                        const uint16_t* q_s, const uint16_t* k_s, const uint16_t* v_s,
+                                        uint16_t* k_cache, uint16_t* v_cache,
+                                        uint16_t* out, float* lse, void* stream);
 
 /* Profiling hook for callers that time the step's kernels.  events: NULL (off)
  * or 4 hipEvent_t created by the caller; each entry may be NULL.  Until the

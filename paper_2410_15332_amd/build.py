@@ -20,7 +20,7 @@ PROBE_SRC = os.path.join(PKG, "probe", "mfma_peak.hip")
 PROBE_LIB = os.path.join(PKG, "probe", "libepic_probe.so")
 
 SOURCES = ["status.cpp", "plan.cpp", "api.cpp", "model.cpp", "link_write.hip", "attention.hip", "gemm.hip",
-           "layer.hip", "decode_attention.hip"]
+           "layer.hip", "decode_attention.hip", "noalloc.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed fp32 VALU forms are disabled: hipcc must not emit them for this target.

@@ -118,6 +118,9 @@ _link_attention = _proto("epic_link_attention", C.c_int,
                          [_P(epic_attn_cfg), _P(epic_plan_sizes), _P(epic_plan), C.c_void_p, C.c_void_p,
                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
                           C.c_void_p])
+_link_attention_noalloc = _proto("epic_link_attention_noalloc", C.c_int,
+                                 [_P(epic_attn_cfg), _P(epic_plan_sizes), _P(epic_plan), C.c_void_p, C.c_void_p,
+                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p])
 _set_prof = _proto("epic_set_profile_events", C.c_int, [C.c_void_p])
 _model_ws = _proto("epic_model_workspace_bytes", C.c_size_t, [_P(epic_model_cfg), _P(epic_plan_sizes)])
 _link_layer = _proto("epic_link_layer", C.c_int,
@@ -137,7 +140,9 @@ EXPORTED = ["epic_status_string", "epic_last_error", "epic_version", "epic_plan_
             "epic_plan_link", "epic_link_workspace_bytes", "epic_link_attention", "epic_set_profile_events",
             "epic_model_workspace_bytes", "epic_link_layer", "epic_link_model", "epic_gemm_workspace_bytes",
             "epic_gemm", "epic_plan_decode_sizes", "epic_plan_decode", "epic_plan_compile_sizes",
-            "epic_plan_compile"]
+            "epic_plan_compile", "epic_link_attention_noalloc"]
+
+NOALLOC_SCRATCH_BYTES = 96 << 20      # EPIC_NOALLOC_SCRATCH_BYTES
 
 GEMM_STORE, GEMM_RESIDUAL, GEMM_SWIGLU = 0, 1, 2
 
@@ -312,6 +317,15 @@ def epic_link_attention(cfg: epic_attn_cfg, dplan: DevicePlan, q_s, k_s, v_s, k_
     _check(_link_attention(C.byref(cfg), C.byref(dplan.sizes), C.byref(dplan.plan), _ptr(q_s), _ptr(k_s),
                            _ptr(v_s), _ptr(k_cache), _ptr(v_cache), _ptr(out), _ptr(lse), _ptr(workspace),
                            ws_bytes, _stream(stream)), "epic_link_attention")
+
+
+def epic_link_attention_noalloc(cfg: epic_attn_cfg, dplan: DevicePlan, q_s, k_s, v_s, k_cache, v_cache, out, lse,
+                                stream=None):
+    """epic_link_attention without a workspace: split-KV partials in the library's fixed
+    device array (see include/epic_link.h)."""
+    _check(_link_attention_noalloc(C.byref(cfg), C.byref(dplan.sizes), C.byref(dplan.plan), _ptr(q_s), _ptr(k_s),
+                                   _ptr(v_s), _ptr(k_cache), _ptr(v_cache), _ptr(out), _ptr(lse), _stream(stream)),
+           "epic_link_attention_noalloc")
 
 
 def epic_set_profile_events(events=None):
