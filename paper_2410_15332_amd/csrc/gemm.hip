@@ -6,6 +6,8 @@
 //   kStoreF32 : C -> fp32 [M][N]                     (Q/K/V projections, Sec. 4.2)
 //   kResidual : h[M][N] += C                         (W_O and W_down; fp32 residual stream)
 //   kSwiGLU   : act[M][N/2] = silu(gate) * up, bf16  (W_gate_up; gate rows [0, F), up rows [F, 2F))
+//   kRope     : the fused Q|K|V projection: q and k heads rotated at each row's linked
+//               position (rotary pairs (i, i + D/2)), v heads as they are; bf16 q, k, v
 //
 // Tiling: workgroup tile 256 x TN, 8 wavefronts of 64 columns each (TN = 256:
 // 2 x 4 wavefronts of 128 x 64, i.e. 4 x 2 v_mfma_f32_32x32x16_bf16 tiles; TN = 128:
@@ -16,7 +18,12 @@
 // instruction fills one group (1 KB) and the 16 lanes of each ds_read_b128 group
 // touch distinct banks.  For kSwiGLU the TN weight rows of a tile are gate/up in
 // 32-row groups (gate j.., up j.., gate j+32.., ...), so a wavefront's two
-// 32-column MFMA tiles hold gate and up of the same 32 outputs.
+// 32-column MFMA tiles hold gate and up of the same 32 outputs.  For kRope the two
+// 32-column MFMA tiles of a wavefront hold the two halves of rotary pairs: with
+// D = 64 that is the natural order (a wavefront's 64 columns are one head); with
+// D = 128 each 128-column head is staged as (i.., i+64.., i+32.., i+96..) in
+// 32-row groups, i = 0.., so lane column c of tile 0 and tile 1 are head
+// columns ip and ip + 64.
 //
 // Scheduling: at most one workgroup per CU (G of them), persistent.  With at least
 // a round of 256 x 256 tiles, whole tiles are dealt in rounds of G, G chosen so the
@@ -174,7 +181,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
       if (a_wave) gr = min(mt * kTM + row, g.M - 1);
       else if constexpr (EPI == kSwiGLU)
         gr = ((row >> 5) & 1) * g.ffn + nt * (TN / 2) + (row >> 6) * 32 + (row & 31);
-      else gr = min(nt * TN + row, g.N - 1);
+      else if constexpr (EPI == kRope) {
+        // D = 128: LDS row p = wn' * 64 + j * 32 + r of a head holds head column
+        // j * 64 + wn' * 32 + r (wn' = wavefront column half within the head)
+        const int hc = g.head_dim == 128 ? (row & ~127) + ((row >> 5) & 1) * 64 + ((row >> 6) & 1) * 32 + (row & 31)
+                                         : row;
+        gr = min(nt * TN + hc, g.N - 1);
+      } else gr = min(nt * TN + row, g.N - 1);
       vo[i] = gr * row_bytes + lchunk * 16;
     }
   };
@@ -245,6 +258,43 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
           const float act = gt * __builtin_amdgcn_rcpf(1.0f + fast_exp2(-gt * kLog2e)) * up;
           __builtin_amdgcn_raw_buffer_store_b16(uint16_t(pack_bf16x2(act, 0.0f) & 0xFFFFu), ro, (m * g.ffn + n) * 2,
                                                 0, 0);
+        }
+    } else if constexpr (EPI == kRope) {
+      // this wavefront's 64 columns: one head (D = 64) or half of one (D = 128, the
+      // pairs ip, ip + 64 with ip in [32 (wn % 2), + 32))
+      const int D = g.head_dim, half = D >> 1;
+      const int head = D == 128 ? (nt * TN >> 7) + (wn >> 1) : (nt * TN >> 6) + wn;
+      if (head >= g.hq + 2 * g.hkv) return;               // columns past N
+      const int ip = (D == 128 ? (wn & 1) * 32 : 0) + col;
+      uint16_t* base;
+      int heads, hd;
+      bool rotate = true;
+      if (head < g.hq) {
+        base = g.q, heads = g.hq, hd = head;
+      } else if (head < g.hq + g.hkv) {
+        base = g.k, heads = g.hkv, hd = head - g.hq;
+      } else {
+        base = g.v, heads = g.hkv, hd = head - g.hq - g.hkv, rotate = false;
+      }
+      const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(base, 0, g.M * heads * D * 2, kBufWord3);
+      const __amdgpu_buffer_rsrc_t rc =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<float2*>(g.cs), 0, g.M * half * 8, kBufWord3);
+#pragma unroll
+      for (int ii = 0; ii < CT / J; ++ii)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + (h * (CT / J) + ii) * 32 + (r >> 2) * 8 + (r & 3);
+          const float x1 = v[ii * J + 0][r], x2 = v[ii * J + 1][r];
+          float y1 = x1, y2 = x2;
+          if (rotate) {
+            const float2 t = __builtin_bit_cast(
+                float2, __builtin_amdgcn_raw_buffer_load_b64(rc, (m * half + ip) * 8, 0, 0));
+            y1 = x1 * t.x - x2 * t.y;
+            y2 = x2 * t.x + x1 * t.y;
+          }
+          const int e = ((m * heads + hd) * D + ip) * 2;
+          __builtin_amdgcn_raw_buffer_store_b16(uint16_t(pack_bf16x2(y1, 0.0f) & 0xFFFFu), ro, e, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b16(uint16_t(pack_bf16x2(y2, 0.0f) & 0xFFFFu), ro, e + half * 2, 0, 0);
         }
     } else {
       if (nt * TN + wn * 64 >= g.N) return;                // this wavefront's columns are past N
@@ -492,6 +542,8 @@ void launch_gemm(const GemmArgs& g, int epi, hipStream_t stream) {
   if (g.M == 0) return;
   if (epi == kStoreF32)
     launch_epi<kStoreF32>(g, stream);
+  else if (epi == kRope)
+    launch_epi<kRope>(g, stream);
   else if (epi == kResidual)
     launch_epi<kResidual>(g, stream);
   else

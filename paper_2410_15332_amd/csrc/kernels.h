@@ -41,7 +41,5 @@ void launch_link_combine(const AttnArgs& a, int head_dim, int n_tiles, hipStream
 void launch_rmsnorm(const float* x, const uint16_t* w, uint16_t* out_bf16, float* out_f32, int rows, int hidden,
                     float eps, hipStream_t stream);
 void launch_rope_table(const int32_t* s_pos, float2* cs, int rows, int head_dim, double theta, hipStream_t stream);
-void launch_rope_split(const float* qkv, const float2* cs, uint16_t* q, uint16_t* k, uint16_t* v, int rows, int hq,
-                       int hkv, int head_dim, hipStream_t stream);
 
 }  // namespace epic

@@ -1,6 +1,6 @@
-// Elementwise parts of a decoder layer for the selected rows: RMSNorm, the
-// rotary table at linked positions, and the rotation / bf16 split of the fused
-// Q|K|V projection.
+// Elementwise parts of a decoder layer for the selected rows: RMSNorm and the
+// rotary table at linked positions (the rotation itself runs in the epilogue of
+// the fused Q|K|V projection, gemm.hip).
 //
 // RMSNorm: y = x / sqrt(mean(x^2) + eps) * w, fp32 statistics.
 // Rotary embedding: the pair (i, i + D/2) of a head is rotated by angle
@@ -74,37 +74,6 @@ __global__ void rope_table_kernel(const int32_t* __restrict__ s_pos, float2* __r
   cs[idx] = make_float2(float(c), float(s));
 }
 
-// qkv fp32 [n][(hq + 2 hkv) D] -> q, k rotated, v copied, all bf16 [n][heads][D].
-// One thread per rotation pair; grid covers n * (hq + 2 hkv) * D/2 pairs.
-__global__ void rope_split_kernel(const float* __restrict__ qkv, const float2* __restrict__ cs,
-                                  uint16_t* __restrict__ q, uint16_t* __restrict__ k, uint16_t* __restrict__ v,
-                                  int n_rows, int hq, int hkv, int D) {
-  const int half = D / 2;
-  const int heads = hq + 2 * hkv;
-  const long idx = long(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (idx >= long(n_rows) * heads * half) return;
-  const int i = int(idx % half);
-  const int hd = int((idx / half) % heads);
-  const int row = int(idx / (long(half) * heads));
-  const float* src = qkv + (size_t(row) * heads + hd) * D;
-  const float x1 = src[i], x2 = src[i + half];
-  float y1 = x1, y2 = x2;
-  if (hd < hq + hkv) {                       // q and k heads rotate, v heads do not
-    const float2 t = cs[size_t(row) * half + i];
-    y1 = x1 * t.x - x2 * t.y;
-    y2 = x2 * t.x + x1 * t.y;
-  }
-  uint16_t* dst;
-  if (hd < hq)
-    dst = q + (size_t(row) * hq + hd) * D;
-  else if (hd < hq + hkv)
-    dst = k + (size_t(row) * hkv + (hd - hq)) * D;
-  else
-    dst = v + (size_t(row) * hkv + (hd - hq - hkv)) * D;
-  dst[i] = uint16_t(pack_bf16x2(y1, 0.0f) & 0xFFFFu);
-  dst[i + half] = uint16_t(pack_bf16x2(y2, 0.0f) & 0xFFFFu);
-}
-
 }  // namespace
 
 void launch_rmsnorm(const float* x, const uint16_t* w, uint16_t* out_bf16, float* out_f32, int rows, int hidden,
@@ -117,13 +86,6 @@ void launch_rope_table(const int32_t* s_pos, float2* cs, int rows, int head_dim,
   const int n = rows * (head_dim / 2);
   if (n == 0) return;
   rope_table_kernel<<<(n + 255) / 256, 256, 0, stream>>>(s_pos, cs, rows, head_dim / 2, std::log2(theta));
-}
-
-void launch_rope_split(const float* qkv, const float2* cs, uint16_t* q, uint16_t* k, uint16_t* v, int rows, int hq,
-                       int hkv, int head_dim, hipStream_t stream) {
-  const long n = long(rows) * (hq + 2 * hkv) * (head_dim / 2);
-  if (n == 0) return;
-  rope_split_kernel<<<unsigned((n + 255) / 256), 256, 0, stream>>>(qkv, cs, q, k, v, rows, hq, hkv, head_dim);
 }
 
 }  // namespace epic

@@ -2,8 +2,8 @@
 //
 // Per layer (Sec. 4.2 recipe inside a Llama-style pre-norm block):
 //   x = RMSNorm(h) w_attn                       bf16
-//   qkv = x Wqkv^T                               fp32   (Q = E W_Q, K = E W_K, V = E W_V)
-//   q, k = RoPE at linked positions; v           bf16
+//   q, k, v = x Wqkv^T, q and k rotated at the     bf16   (Q = E W_Q, K = E W_K, V = E W_V;
+//             rows' linked positions                   one GEMM, rotation in its epilogue)
 //   link write + attention over K_exp / V_exp    bf16   (Eq. 1)
 //   h += o Wo^T                                  fp32   (O = A V_exp W_O, residual)
 //   x = RMSNorm(h) w_mlp;  h += (silu(x Wg^T) * (x Wu^T)) Wd^T
@@ -28,7 +28,6 @@ size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 
 struct LayerWs {
   uint16_t* x;       // [n_s][hidden]
-  float* qkv;        // [n_s][(hq + 2 hkv) D]
   uint16_t* q;       // [n_s][hq][D]
   uint16_t* k;       // [n_s][hkv][D]
   uint16_t* v;       // [n_s][hkv][D]
@@ -52,7 +51,6 @@ LayerWs carve(const epic_model_cfg* c, const epic_plan_sizes* s, char* base) {
     return p;
   };
   w.x = reinterpret_cast<uint16_t*>(take(n * c->hidden * 2));
-  w.qkv = reinterpret_cast<float*>(take(n * size_t(hq + 2 * hkv) * D * 4));
   w.q = reinterpret_cast<uint16_t*>(take(n * size_t(hq) * D * 2));
   w.k = reinterpret_cast<uint16_t*>(take(n * size_t(hkv) * D * 2));
   w.v = reinterpret_cast<uint16_t*>(take(n * size_t(hkv) * D * 2));
@@ -108,14 +106,19 @@ epic_status run_layer(const epic_model_cfg* c, const epic_layer_weights* w, cons
   GemmArgs g{};
   g.A = ws.x;
   g.W = w->wqkv;
-  g.C = ws.qkv;
   g.M = n;
   g.N = (hq + 2 * hkv) * D;
   g.K = H;
+  g.q = ws.q;
+  g.k = ws.k;
+  g.v = ws.v;
+  g.cs = ws.cs;
+  g.hq = hq;
+  g.hkv = hkv;
+  g.head_dim = D;
   g.partial = ws.gemm_partial;
   g.tile_count = ws.gemm_count;
-  launch_gemm(g, kStoreF32, stream);
-  launch_rope_split(ws.qkv, ws.cs, ws.q, ws.k, ws.v, n, hq, hkv, D, stream);
+  launch_gemm(g, kRope, stream);
   epic_attn_cfg ac = c->attn;
   ac.rope_theta = c->rope_theta;            // cached K was rotated with the model's base
   epic_status st = run_link_attention(&ac, s, p, ws.q, ws.k, ws.v, kc, vc, ws.o, nullptr, ws.attn, stream);
