@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build", "epic_link")
 LIB = os.path.join(PKG, "libepic_link.so")
 # measurement tooling, outside the product library: the MFMA throughput probe
-PROBE_SRC = os.path.join(PKG, "probe", "mfma_peak.hip")
+PROBE_SRC = [os.path.join(PKG, "probe", f) for f in ("mfma_peak.hip", "coexec.hip")]
 PROBE_LIB = os.path.join(PKG, "probe", "libepic_probe.so")
 
 SOURCES = ["status.cpp", "plan.cpp", "api.cpp", "model.cpp", "link_write.hip", "attention.hip", "gemm.hip",
@@ -52,7 +52,7 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
     tmp = PROBE_LIB + ".tmp"
-    cmd = [HIPCC, "-x", "hip", f"--offload-arch={ARCH}", *DEVICE_FLAGS, *COMMON, "-shared", PROBE_SRC, "-o", tmp]
+    cmd = [HIPCC, "-x", "hip", f"--offload-arch={ARCH}", *DEVICE_FLAGS, *COMMON, "-shared", *PROBE_SRC, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"probe build failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

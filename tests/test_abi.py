@@ -51,8 +51,12 @@ def test_probe_library_exports_what_bench_calls():
     arguments on the host before any launch."""
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2410_15332_amd", "probe", "libepic_probe.so"))
     for name in ("epic_probe_mfma_bf16", "epic_probe_mfma_bf16_varied", "epic_probe_mfma_bf16_flops",
-                 "epic_probe_hbm_read"):
+                 "epic_probe_hbm_read", "epic_probe_coexec", "epic_probe_coexec_iters"):
         assert hasattr(lib, name), name
+    lib.epic_probe_coexec.restype = ctypes.c_int
+    lib.epic_probe_coexec.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p] * 3
+    assert lib.epic_probe_coexec(1, 32, 1, 256, None, None, None) != 0       # no buffers
+    assert lib.epic_probe_coexec(1, 24, 1, 256, 16, 16, None) != 0           # not a built variant
     lib.epic_probe_mfma_bf16_flops.restype = ctypes.c_double
     lib.epic_probe_mfma_bf16_flops.argtypes = [ctypes.c_int, ctypes.c_int]
     assert lib.epic_probe_mfma_bf16_flops(2, 3) == 2 * 8 * 3 * 4 * 2.0 * 32 * 32 * 16
