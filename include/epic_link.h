@@ -343,7 +343,7 @@ epic_status epic_link_model(const epic_model_cfg* cfg, const epic_layer_weights*
  *          EPIC_GEMM_RESIDUAL: c[i][j] += C[i][j]                      c: fp32 [m][n], in place
  *          EPIC_GEMM_SWIGLU:   act[i][j] = bf16(silu(C[i][j]) C[i][j + n/2]), j < n/2
  *                              (rows [0, n/2) of w: gate; [n/2, n): up)   act: bf16 [m][n/2]
- * Shapes: m >= 0, k % 32 == 0, n % 128 == 0, and with m rounded up to a multiple
+ * Shapes: m >= 0, k % 64 == 0, n % 128 == 0, and with m rounded up to a multiple
  * of 256 every operand and output below 2^31 bytes; else EPIC_ERR_UNSUPPORTED.
  * Device pointers, 16-byte aligned.  workspace: at least epic_gemm_workspace_bytes()
  * bytes of device memory, 256-byte aligned, owned by the caller; it holds the

@@ -26,7 +26,7 @@ struct GemmArgs {
   float* partial;      // split-tile partial sums, gemm_workspace_bytes() with tile_count
   int* tile_count;     // arrival counters of split tiles (per wavefront); zero before the first launch
 };
-// Requirements: K % 32 == 0; N % 128 == 0 (kStoreF32 / kResidual / kRope); ffn % 128 == 0
+// Requirements: K % 64 == 0; N % 128 == 0 (kStoreF32 / kResidual / kRope); ffn % 128 == 0
 // (kSwiGLU); head_dim 64 or 128 (kRope); M * K and N * K below 2^30 (byte offsets of the
 // operands fit 31 bits).
 

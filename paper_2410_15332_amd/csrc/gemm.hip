@@ -11,10 +11,12 @@
 //
 // Tiling: workgroup tile 256 x TN, 8 wavefronts of 64 columns each (TN = 256:
 // 2 x 4 wavefronts of 128 x 64, i.e. 4 x 2 v_mfma_f32_32x32x16_bf16 tiles; TN = 128:
-// 4 x 2 wavefronts of 64 x 64).  K runs in stages of 32 staged in LDS by direct
-// buffer->LDS loads, NS stages in LDS (4 at TN = 256, 6 at TN = 128; loads issued
-// NS - 1 stages ahead of use).  An operand stage is 16 groups of 16 rows; row r of a group sits at
-// byte 64 r with its four 16-byte chunks XOR-swizzled by (r / 4) % 4, so one load
+// 4 x 2 wavefronts of 64 x 64).  K runs in stages of 64 staged in LDS by direct
+// buffer->LDS loads, NS stages in LDS (2 at TN = 256, 3 at TN = 128; loads issued
+// NS - 1 stages ahead of use).  An operand stage is groups of 8 rows of 128 bytes
+// (one whole cache line per row: a load instruction that covers 16 half lines moves
+// about 0.6x the bytes per cycle of one that covers 8 whole lines); row r sits at byte
+// 128 r with its eight 16-byte chunks XOR-swizzled by (r / 2) % 8, so one load
 // instruction fills one group (1 KB) and the 16 lanes of each ds_read_b128 group
 // touch distinct banks.  For kSwiGLU the TN weight rows of a tile are gate/up in
 // 32-row groups (gate j.., up j.., gate j+32.., ...), so a wavefront's two
@@ -48,25 +50,26 @@ namespace epic {
 
 namespace {
 
-constexpr int kTM = 256, kBK = 32;
+constexpr int kTM = 256, kBK = 64;
 constexpr int kThreads = 512;
 constexpr int kBufWord3 = 0x00020000;                   // gfx9 raw buffer descriptor word 3
 constexpr int kMaxWorkers = 256;                        // one workgroup per CU
 constexpr int kPartialFloats = kTM * 256;               // fp32 partial sums of the largest tile
 constexpr int kMaxSplitTiles = 2 * kMaxWorkers;
 constexpr int kCounters = kMaxSplitTiles * (kThreads / 64);   // one per (cut tile, wavefront)
-constexpr int kMinUnits = 8;                            // K stages per workgroup, at least
+constexpr int kMinUnits = 4;                            // K stages per workgroup, at least
 
 template <int TN>
 struct Shape {
-  static constexpr int NS = TN == 256 ? 4 : 6;          // LDS stages (128 / 144 KB)
+  static constexpr int NS = TN == 256 ? 2 : 3;          // LDS stages (128 / 144 KB)
   static constexpr int WAVES_M = TN == 256 ? 2 : 4;     // wavefronts along M
   static constexpr int WM = kTM / WAVES_M;              // rows per wavefront
   static constexpr int I = WM / 32;                     // 32-row MFMA tiles per wavefront
   static constexpr int J = 2;                           // 32-column MFMA tiles per wavefront
   static constexpr int A_STAGE = kTM * kBK * 2;         // bytes per stage
   static constexpr int B_STAGE = TN * kBK * 2;
-  static constexpr int NLB = TN / 64;                   // W row groups per loading wavefront
+  static constexpr int NLA = kTM / 32;                  // A row groups (8 rows) per loading wavefront
+  static constexpr int NLB = TN / 32;                   // W row groups per loading wavefront
 };
 
 struct GemmPlan {
@@ -84,6 +87,13 @@ struct GemmLds {
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
+
+// One 16-byte-per-lane buffer->LDS load (1 KB per wavefront: lane l's 16 bytes land
+// at dst + 16 l).  A plain function, so the call is never a template-dependent
+// expression (the host pass cannot check this builtin inside a template).
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, char* dst, int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)dst, 16, voff, soff, 0, 0);
+}
 
 // Workgroup barrier ordering LDS accesses only (waits for this wavefront's LDS
 // reads, not for its buffer->LDS loads still in flight).
@@ -107,7 +117,7 @@ struct Cursor {
 template <int EPI, int TN>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan p) {
   using SH = Shape<TN>;
-  constexpr int NS = SH::NS, I = SH::I, J = SH::J;
+  constexpr int NS = SH::NS, I = SH::I, J = SH::J, NLA = SH::NLA;
   __shared__ __attribute__((aligned(1024))) GemmLds<TN> lds;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -156,27 +166,27 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     if (++c.kt == c.kend) seek(c, c.u);
   };
 
-  // ---- buffer->LDS loads: wavefronts 0..3 stage the 16 A row groups (4 each),
-  // 4..7 the TN / 16 W row groups (NLB each).
+  // ---- buffer->LDS loads: wavefronts 0..3 stage the 32 A row groups (8 each),
+  // 4..7 the TN / 8 W row groups (NLB each).
   const bool a_wave = wv < 4;
-  // With M <= 128 (one row tile) the A row groups 8..15 hold no row of A: their
+  // With M <= 128 (one row tile) the A row groups 16..31 hold no row of A: their
   // loading wavefronts issue nothing (none of their waits then has anything to wait for).
   const bool dma_idle = TN == 128 && a_wave && g.M <= 128 && wv >= 2;
-  const int nl = a_wave ? 4 : SH::NLB;                     // loads per stage of this wavefront
+  const int nl = a_wave ? NLA : SH::NLB;               // loads per stage of this wavefront
   const int grp0 = nl * (wv & 3);
-  const int lrow = lane >> 2;                              // row within a 16-row group
-  const int lchunk = (lane & 3) ^ ((lane >> 4) & 3);       // 16-byte chunk of that row this lane loads
+  const int lrow = lane >> 3;                              // row within an 8-row group
   const int row_bytes = g.K * 2;
   const int w_rows = EPI == kSwiGLU ? 2 * g.ffn : g.N;
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a_wave ? g.A : g.W), 0, (a_wave ? g.M : w_rows) * row_bytes, kBufWord3);
-  int vo[4];                                               // lane byte offsets of the row groups
+  int vo[kTM / 32];                                     // lane byte offsets of the row groups (NLA)
   auto dma_setup = [&](int tile) __attribute__((always_inline)) {
     int mt, nt;
     tile_mn(tile, mt, nt);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = (grp0 + i) * 16 + lrow;              // row of the operand tile
+    for (int i = 0; i < NLA; ++i) {
+      const int row = (grp0 + i) * 8 + lrow;               // row of the operand tile
+      const int lchunk = (lane & 7) ^ ((row >> 1) & 7);    // 16-byte chunk of that row this lane loads
       int gr;
       if (a_wave) gr = min(mt * kTM + row, g.M - 1);
       else if constexpr (EPI == kSwiGLU)
@@ -197,30 +207,33 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     if (dma_idle) return;
     char* dst = dma_base + buf * dma_stage;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < NLA; ++i)
       if (i < SH::NLB || a_wave)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + i * 1024), 16, vo[i], kt * (kBK * 2), 0, 0);
+        dma16(rs, dst + i * 1024, vo[i], kt * (kBK * 2));
   };
 
-  // ---- MFMA operands: lane l reads row l % 32 of a 32-row tile, 16-byte chunk
-  // 2 ks + l / 32 of the stage, stored at chunk position chunk ^ ((l % 16) / 4).
-  const int lrow16 = ((lane >> 4) & 1) * 1024 + (lane & 15) * 64;
-  const int lb0 = lrow16 + (((lane >> 5) ^ ((lane >> 2) & 3)) * 16);
-  const int lb1 = lrow16 + (((2 + (lane >> 5)) ^ ((lane >> 2) & 3)) * 16);
-  const char* const pa0 = lds.a[0] + wm * (SH::WM / 16) * 1024 + lb0;
-  const char* const pa1 = lds.a[0] + wm * (SH::WM / 16) * 1024 + lb1;
-  const char* const pb0 = lds.b[0] + wn * 4096 + lb0;
-  const char* const pb1 = lds.b[0] + wn * 4096 + lb1;
+  // ---- MFMA operands: for k-slice ks (16 wide, 4 per stage) lane l reads row l % 32
+  // of a 32-row tile, 16-byte chunk 2 ks + l / 32, stored at chunk position
+  // chunk ^ ((l % 32) / 2 % 8).
+  const int lrow32 = (lane & 31) * 128;
+  const int lsw = (lane >> 1) & 7;
+  const int lb0 = lrow32 + (((0 + (lane >> 5)) ^ lsw) * 16);
+  const int lb1 = lrow32 + (((2 + (lane >> 5)) ^ lsw) * 16);
+  const int lb2 = lrow32 + (((4 + (lane >> 5)) ^ lsw) * 16);
+  const int lb3 = lrow32 + (((6 + (lane >> 5)) ^ lsw) * 16);
+  const char* const pa = lds.a[0] + wm * SH::WM * 128;
+  const char* const pb = lds.b[0] + wn * 64 * 128;
   struct Frags {
     bf16x8 a[I], b[J];
   };
   auto read = [&](Frags& f, int buf, int ks) __attribute__((always_inline)) {
-    const char* pa = (ks ? pa1 : pa0) + buf * SH::A_STAGE;
-    const char* pb = (ks ? pb1 : pb0) + buf * SH::B_STAGE;
+    const int lb = ks == 0 ? lb0 : ks == 1 ? lb1 : ks == 2 ? lb2 : lb3;
+    const char* a = pa + buf * SH::A_STAGE + lb;
+    const char* b = pb + buf * SH::B_STAGE + lb;
 #pragma unroll
-    for (int i = 0; i < I; ++i) f.a[i] = *reinterpret_cast<const bf16x8*>(pa + i * 2048);
+    for (int i = 0; i < I; ++i) f.a[i] = *reinterpret_cast<const bf16x8*>(a + i * 4096);
 #pragma unroll
-    for (int j = 0; j < J; ++j) f.b[j] = *reinterpret_cast<const bf16x8*>(pb + j * 2048);
+    for (int j = 0; j < J; ++j) f.b[j] = *reinterpret_cast<const bf16x8*>(b + j * 4096);
   };
 
   f32x16 acc[I][J];
@@ -280,22 +293,30 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
       const __amdgpu_buffer_rsrc_t rc =
           __builtin_amdgcn_make_buffer_rsrc(const_cast<float2*>(g.cs), 0, g.M * half * 8, kBufWord3);
 #pragma unroll
-      for (int ii = 0; ii < CT / J; ++ii)
+      for (int ii = 0; ii < CT / J; ++ii) {
+        // the row block's cos / sin first, so the 16 loads are in flight together (a
+        // load is not moved above an earlier buffer store)
+        float2 t[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + (h * (CT / J) + ii) * 32 + (r >> 2) * 8 + (r & 3);
+          t[r] = rotate ? __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(rc, (m * half + ip) * 8, 0, 0))
+                        : make_float2(1.0f, 0.0f);
+        }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int m = m0 + (h * (CT / J) + ii) * 32 + (r >> 2) * 8 + (r & 3);
           const float x1 = v[ii * J + 0][r], x2 = v[ii * J + 1][r];
           float y1 = x1, y2 = x2;
           if (rotate) {
-            const float2 t = __builtin_bit_cast(
-                float2, __builtin_amdgcn_raw_buffer_load_b64(rc, (m * half + ip) * 8, 0, 0));
-            y1 = x1 * t.x - x2 * t.y;
-            y2 = x2 * t.x + x1 * t.y;
+            y1 = x1 * t[r].x - x2 * t[r].y;
+            y2 = x2 * t[r].x + x1 * t[r].y;
           }
           const int e = ((m * heads + hd) * D + ip) * 2;
           __builtin_amdgcn_raw_buffer_store_b16(uint16_t(pack_bf16x2(y1, 0.0f) & 0xFFFFu), ro, e, 0, 0);
           __builtin_amdgcn_raw_buffer_store_b16(uint16_t(pack_bf16x2(y2, 0.0f) & 0xFFFFu), ro, e + half * 2, 0, 0);
         }
+      }
     } else {
       if (nt * TN + wn * 64 >= g.N) return;                // this wavefront's columns are past N
       const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(g.C, 0, g.M * g.N * 4, kBufWord3);
@@ -411,7 +432,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   };
 
   // ---- pipeline: unit u (one K stage of one tile) lives in LDS buffer u % NS.
-  // Step u reads its second k-slice while the first runs on the matrix cores,
+  // Step u reads each k-slice while the previous one runs on the matrix cores,
   // waits for this wavefront's loads of unit u + 1, and after the barrier (all
   // loads of u + 1 visible, every read of buffer u % NS done) refills that buffer
   // with unit u + NS and reads the first k-slice of u + 1.  Loads past the last
@@ -432,7 +453,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   };
 #pragma unroll
   for (int b = 0; b < NS; ++b) dma_next(b);
-  if (a_wave) wait_vmem<(NS - 1) * 4>();            // unit 0 of this wavefront
+  if (a_wave) wait_vmem<(NS - 1) * NLA>();      // unit 0 of this wavefront
   else wait_vmem<(NS - 1) * SH::NLB>();
   barrier_lds();                                    // ... of every wavefront
   Frags f0, f1;
@@ -456,8 +477,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
       if (live) {
         read(f1, buf, 1);
         mma(f0);
+        read(f0, buf, 2);
+        mma(f1);
+        read(f1, buf, 3);
+        mma(f0);
       }
-      if (a_wave) wait_vmem<(NS - 2) * 4>();        // this wavefront's loads of unit u + 1
+      if (a_wave) wait_vmem<(NS - 2) * NLA>();  // this wavefront's loads of unit u + 1
       else wait_vmem<(NS - 2) * SH::NLB>();
       barrier_lds();
       dma_next(buf);

@@ -262,8 +262,8 @@ extern "C" epic_status epic_gemm(int32_t epilogue, const uint16_t* a, const uint
   clear_error();
   EPIC_CHECK_ARG(epilogue >= EPIC_GEMM_STORE && epilogue <= EPIC_GEMM_SWIGLU, "unknown epilogue %d", epilogue);
   EPIC_CHECK_ARG(m >= 0 && n > 0 && k > 0, "m, n, k = %d, %d, %d", m, n, k);
-  if (k % 32 != 0 || n % 128 != 0)
-    return fail(EPIC_ERR_UNSUPPORTED, "k %% 32 == 0 and n %% 128 == 0 required (k = %d, n = %d)", k, n);
+  if (k % 64 != 0 || n % 128 != 0)
+    return fail(EPIC_ERR_UNSUPPORTED, "k %% 64 == 0 and n %% 128 == 0 required (k = %d, n = %d)", k, n);
   const int64_t rows = int64_t(m) + 256, lim = int64_t(1) << 31;
   const int64_t out_row_bytes = epilogue == EPIC_GEMM_SWIGLU ? int64_t(n / 2) * 2 : int64_t(n) * 4;
   if (rows * k * 2 >= lim || int64_t(n) * k * 2 >= lim || rows * out_row_bytes >= lim)

@@ -95,7 +95,7 @@ def test_large_row_counts_sampled(m, n, k, epi):
 
 
 SMALL = [
-    (1, 128, 32, "store"),
+    (1, 128, 64, "store"),
     (28, 384, 256, "residual"),
     (200, 768, 512, "store"),
     (255, 384, 640, "swiglu"),          # ffn = 192: 64-column SwiGLU tiles
@@ -125,10 +125,15 @@ def test_empty_and_rejected_shapes():
     el.epic_gemm(el.GEMM_STORE, a, w, c=c, workspace=ws)          # m = 0: nothing to do
     a = torch.zeros((4, 48), dtype=torch.bfloat16, device="cuda")
     w = torch.zeros((128, 48), dtype=torch.bfloat16, device="cuda")
-    with pytest.raises(el.EpicError) as e:                         # k % 32 != 0
+    with pytest.raises(el.EpicError) as e:                         # k % 64 != 0
         el.epic_gemm(el.GEMM_STORE, a, w, c=torch.zeros((4, 128), device="cuda"), workspace=ws)
     assert e.value.status == 2
-    with pytest.raises(el.EpicError) as e:                         # workspace too small
+    with pytest.raises(el.EpicError) as e:                         # k % 64 != 0
         el.epic_gemm(el.GEMM_STORE, a[:, :32].contiguous(), w[:, :32].contiguous(),
-                     c=torch.zeros((4, 128), device="cuda"), workspace=ws[:1024])
+                     c=torch.zeros((4, 128), device="cuda"), workspace=ws)
+    assert e.value.status == 2
+    a = torch.zeros((4, 64), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((128, 64), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(el.EpicError) as e:                         # workspace too small
+        el.epic_gemm(el.GEMM_STORE, a, w, c=torch.zeros((4, 128), device="cuda"), workspace=ws[:1024])
     assert e.value.status == 4
