@@ -492,6 +492,7 @@ def bench_model(args, wl, n_dummy: int = 0):
     t0 = time.time()
     st = harness.stage_model(wl, caches="compile", weights_on_device=True, n_dummy=n_dummy, tile_rows=args.tile_rows)
     torch.cuda.synchronize()
+    calibration_copy(args.calibrate_copy_mib)
     log(f"staged {wl.name}: n_s={st.sizes.n_s}, {wl.n_layers} layers, chunks compiled on the GPU "
         f"({n_dummy} dummy tokens) in {time.time() - t0:.1f}s")
     for _ in range(args.warmup):

@@ -15,8 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build", "epic_link")
 LIB = os.path.join(PKG, "libepic_link.so")
-# measurement tooling, outside the product library: the MFMA throughput probe
-PROBE_SRC = [os.path.join(PKG, "probe", f) for f in ("mfma_peak.hip", "coexec.hip")]
+# measurement tooling, outside the product library: the MFMA, co-execution and load-path probes
+PROBE_SRC = [os.path.join(PKG, "probe", f) for f in ("mfma_peak.hip", "coexec.hip", "load_path.hip")]
 PROBE_LIB = os.path.join(PKG, "probe", "libepic_probe.so")
 
 SOURCES = ["status.cpp", "plan.cpp", "api.cpp", "model.cpp", "link_write.hip", "attention.hip", "gemm.hip",

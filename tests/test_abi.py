@@ -51,7 +51,8 @@ def test_probe_library_exports_what_bench_calls():
     arguments on the host before any launch."""
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2410_15332_amd", "probe", "libepic_probe.so"))
     for name in ("epic_probe_mfma_bf16", "epic_probe_mfma_bf16_varied", "epic_probe_mfma_bf16_flops",
-                 "epic_probe_hbm_read", "epic_probe_coexec", "epic_probe_coexec_iters"):
+                 "epic_probe_hbm_read", "epic_probe_coexec", "epic_probe_coexec_iters", "epic_probe_load_path",
+                 "epic_probe_load_path_stage_bytes"):
         assert hasattr(lib, name), name
     lib.epic_probe_coexec.restype = ctypes.c_int
     lib.epic_probe_coexec.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p] * 3
@@ -67,3 +68,12 @@ def test_probe_library_exports_what_bench_calls():
     lib.epic_probe_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
                                         ctypes.c_void_p]
     assert lib.epic_probe_hbm_read(None, 16, None, 1, None) != 0            # no buffers
+    lib.epic_probe_load_path.restype = ctypes.c_int
+    lib.epic_probe_load_path.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_int,
+                                         ctypes.c_void_p, ctypes.c_void_p]
+    assert lib.epic_probe_load_path_stage_bytes(1) == 32768
+    assert lib.epic_probe_load_path_stage_bytes(10) == -1                  # no such variant
+    assert lib.epic_probe_load_path(0, None, 1 << 30, 4, 256, 16, None) != 0       # no source
+    assert lib.epic_probe_load_path(0, 16, 1 << 30, 4, 254, 16, None) != 0         # steps not a multiple of 4
+    assert lib.epic_probe_load_path(0, 16, 64 << 20, 4, 256, 16, None) != 0        # source smaller than 32 regions
+    assert lib.epic_probe_load_path(11, 16, 1 << 30, 4, 256, 16, None) != 0        # no such variant
