@@ -135,6 +135,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   const int dp_units = (wr < p.dp_tiles ? (p.dp_tiles - wr + p.G - 1) / p.G : 0) * p.ks;
   const int n_units = dp_units + (s1 - s0);
   if (n_units == 0) return;             // (no such workgroup is launched; kept as a guard)
+  // The K share runs its last segment first: that segment starts a tile (K stage 0)
+  // and the rest ends one (the last stage), so the workgroups of an XCD that cross a
+  // tile boundary sit at two K offsets at any time instead of one each, and their
+  // operand stages are shared in the L2.  sh: first unit of the last segment.
+  const int sh = max(s0, s1 > s0 ? (s1 - 1) / p.ks * p.ks : s0);
 
   auto tile_mn = [&](int t, int& mt, int& nt) __attribute__((always_inline)) {
     const int per_group = p.gm * p.n_tiles;
@@ -152,11 +157,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
       c.kbeg = 0;
       c.kend = p.ks;
     } else {
-      const int v = s0 + (u - dp_units);
+      const int i = u - dp_units;           // position in the share's processing order
+      const bool first = i < s1 - sh;       // in the last segment, run first
+      const int v = first ? sh + i : s0 + (i - (s1 - sh));
       const int q = v / p.ks;
       c.tile = p.dp_tiles + q;
       c.kbeg = v - q * p.ks;
-      c.kend = min(p.ks, s1 - q * p.ks);
+      c.kend = min(p.ks, (first ? s1 : sh) - q * p.ks);
     }
     c.kt = c.kbeg;
   };
