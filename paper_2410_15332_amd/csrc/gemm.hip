@@ -42,6 +42,7 @@
 // on an XCD share operands through its L2.
 // Rows past M and columns past N are computed from clamped rows and never stored.
 #include <algorithm>
+#include <cstdlib>
 
 #include "device_common.h"
 #include "gemm.h"
@@ -78,6 +79,7 @@ struct GemmPlan {
   int G;                       // workgroups
   int dp_rounds, dp_tiles;     // whole-tile rounds and the tiles they cover (tiles 0 .. dp_tiles-1)
   int sk_units;                // K stages of the cut tiles (tiles dp_tiles ..)
+  int polls;                   // counter polls of a cut tile's last-stage owner before it falls back
 };
 
 template <int TN>
@@ -391,6 +393,59 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     };
     constexpr int kSc1 = 16;             // cache policy sc1 alone: agent (device) scope
     typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+    int* cnt = g.tile_count + q * (kThreads / 64) + wv;
+    // Sum of the partials of workers wf .. x1 in K order, plus this wavefront's own
+    // accumulators last (own: the owner of the tile's last stage), then the epilogue.
+    auto fixup = [&](int x1, bool own) __attribute__((always_inline)) {
+#pragma unroll
+      for (int h = 0; h < NCH; ++h) {
+        f32x16 v[CT];
+#pragma unroll
+        for (int t = 0; t < CT; ++t) v[t] = f32x16{};
+        for (int x = wf; x <= x1; ++x) {
+          const int off = slot_off(x);
+#pragma unroll
+          for (int t = 0; t < CT; ++t)
+#pragma unroll
+            for (int qd = 0; qd < 4; ++qd) {
+              const f32x4 p4 = __builtin_bit_cast(
+                  f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off + ((h * CT + t) * 4 + qd) * 1024, 0, kSc1));
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[t][4 * qd + e] += p4[e];
+            }
+        }
+        if (own) {
+#pragma unroll
+          for (int t = 0; t < CT; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) v[t][r] += acc[(h * CT + t) / J][(h * CT + t) % J][r];
+        }
+        epilogue_part(mt, nt, h, v);
+      }
+      if (lane == 0) __hip_atomic_exchange(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);   // ready for the next launch
+    };
+    // The owner of the tile's last stage runs that segment last (its K share runs the
+    // segment that starts a tile first), so the others' partials are usually written
+    // by then: it polls the counter, a bounded number of times, until the other
+    // wl - wf parts have arrived, and finishes from its registers without writing its
+    // own partial.  The others never see the count reach wl - wf before it, so none of
+    // them finishes the tile.  If they are not all there in time it falls back to the
+    // protocol below (write, count, the last to arrive finishes); the sums are the same
+    // on both paths.
+    if (wr == wl) {
+      int seen = 0;
+      for (int it = 0; it < p.polls; ++it) {
+        if (lane == 0) seen = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        seen = __builtin_amdgcn_readfirstlane(seen);
+        if (seen == wl - wf) break;
+        __builtin_amdgcn_s_sleep(2);
+      }
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      if (seen == wl - wf) {
+        fixup(wl - 1, true);
+        return;
+      }
+    }
     const int mine = slot_off(wr);
 #pragma unroll
     for (int t = 0; t < NT; ++t)
@@ -409,33 +464,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     // compiler from moving the stores below it or the partial loads above it (they
     // emit no instruction, so no L2 write-back).
     wait_vmem<0>();                      // this wavefront's partial has landed
-    int* cnt = g.tile_count + q * (kThreads / 64) + wv;
     int before = 0;
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     if (lane == 0) before = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     before = __builtin_amdgcn_readfirstlane(before);
     if (before != wl - wf) return;       // not the last to arrive
-#pragma unroll
-    for (int h = 0; h < NCH; ++h) {      // sum the partials in K order, CT tiles at a time
-      f32x16 v[CT];
-#pragma unroll
-      for (int t = 0; t < CT; ++t) v[t] = f32x16{};
-      for (int x = wf; x <= wl; ++x) {
-        const int off = slot_off(x);
-#pragma unroll
-        for (int t = 0; t < CT; ++t)
-#pragma unroll
-          for (int qd = 0; qd < 4; ++qd) {
-            const f32x4 p4 = __builtin_bit_cast(
-                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off + ((h * CT + t) * 4 + qd) * 1024, 0, kSc1));
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[t][4 * qd + e] += p4[e];
-          }
-      }
-      epilogue_part(mt, nt, h, v);
-    }
-    if (lane == 0) __hip_atomic_exchange(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);   // ready for the next launch
+    fixup(wl, false);                    // the last to arrive: every part from the partials
   };
 
   // ---- pipeline: unit u (one K stage of one tile) lives in LDS buffer u % NS.
@@ -518,6 +553,16 @@ __global__ void gemm_clear_kernel(int* cnt) {
 
 int cdiv(int a, int b) { return (a + b - 1) / b; }
 
+// Counter polls of a cut tile's last-stage owner (about 0.3 ms at the default).  The
+// environment variable EPIC_GEMM_FINISH_POLLS overrides it (0 forces the fallback
+// protocol: a test hook); read at every launch.
+int finish_polls() {
+  const char* e = std::getenv("EPIC_GEMM_FINISH_POLLS");
+  if (e == nullptr || *e == 0) return 4096;
+  const long v = std::strtol(e, nullptr, 10);
+  return int(std::min<long>(std::max<long>(v, 0), 1 << 20));
+}
+
 template <int EPI, int TN>
 void launch_tn(const GemmArgs& g, bool whole_tiles, hipStream_t stream) {
   GemmPlan p{};
@@ -541,6 +586,7 @@ void launch_tn(const GemmArgs& g, bool whole_tiles, hipStream_t stream) {
     p.dp_tiles = p.dp_rounds * p.G;
     p.sk_units = int((tiles - p.dp_tiles) * p.ks);
   }
+  p.polls = finish_polls();
   gemm_kernel<EPI, TN><<<dim3(p.G), kThreads, 0, stream>>>(g, p);
 }
 

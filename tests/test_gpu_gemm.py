@@ -65,6 +65,7 @@ def _run(m, n, k, epi, tag, sample=None):
     bound = (2.0 ** -8) * np.abs(ref) + 1e-4 * s if epi == "swiglu" else 1e-4 * s
     print(f"[gpu-test]   max|err| {err.max():.3e} (scale {s:.3f})", flush=True)
     assert np.all(err <= bound), f"max err {err.max()} at {np.unravel_index(err.argmax(), err.shape)}"
+    return got
 
 
 LINK = [  # the projections of the Llama-3-8B-shaped link step, 736 S rows
@@ -107,6 +108,21 @@ SMALL = [
 @pytest.mark.parametrize("m,n,k,epi", SMALL, ids=[f"{c[3]}_{c[0]}x{c[1]}x{c[2]}" for c in SMALL])
 def test_small_and_ragged(m, n, k, epi):
     _run(m, n, k, epi, tag=20 + SMALL.index((m, n, k, epi)))
+
+
+CUT = [(736, 6144, 4096, "store"), (736, 4096, 14336, "residual"), (300, 1024, 512, "store")]
+
+
+@pytest.mark.parametrize("m,n,k,epi", CUT, ids=[f"{c[3]}_{c[0]}x{c[1]}x{c[2]}" for c in CUT])
+def test_cut_tile_fallback_matches_fast_path(m, n, k, epi, monkeypatch):
+    """A cut tile's last-stage owner finishes from its registers once the other parts
+    have arrived; with no polls allowed (EPIC_GEMM_FINISH_POLLS=0) it always falls back
+    to writing its partial and letting the last to arrive finish.  Both paths sum the
+    same partials in the same K order: bit-identical outputs, each within the bar."""
+    fast = _run(m, n, k, epi, tag=40 + CUT.index((m, n, k, epi)))
+    monkeypatch.setenv("EPIC_GEMM_FINISH_POLLS", "0")
+    slow = _run(m, n, k, epi, tag=40 + CUT.index((m, n, k, epi)))
+    assert np.array_equal(fast, slow)
 
 
 def test_repeated_calls_reuse_workspace():
