@@ -35,8 +35,8 @@
 // per workgroup, so every CU gets the same work.
 // A tile cut across workgroups: each wavefront writes its fp32 partial, bumps its
 // arrival counter for the tile, and the last wavefront to arrive sums that part's
-// partials in K order (the result does not depend on arrival order) and runs its
-// epilogue.  Nothing waits for another workgroup.  Workgroups are dealt round-robin to the 8 XCDs; worker indices are
+// partials in a fixed order (the result does not depend on arrival order) and runs
+// its epilogue.  Nothing waits for another workgroup.  Workgroups are dealt round-robin to the 8 XCDs; worker indices are
 // arranged so that each XCD works on a contiguous run of tiles, and tiles are
 // ordered in groups of up to 8 row tiles per weight tile, so concurrent workgroups
 // on an XCD share operands through its L2.
@@ -264,7 +264,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   // t = i*J + j, register r: row wm*WM + i*32 + (r/4)*8 + half*4 + r%4, column
   // wn*64 + j*32 + col of the workgroup tile.  Written CT tiles (CT / J row blocks)
   // at a time, so the fixup below never holds more than CT tiles of sums.
-  constexpr int NT = I * J, CT = NT == 4 ? 4 : 2, NCH = NT / CT;
+  constexpr int NT = I * J, CT = 2, NCH = NT / CT;
   const int col = lane & 31, half = lane >> 5;
   auto epilogue_part = [&](int mt, int nt, int h, const f32x16 (&v)[CT]) __attribute__((always_inline)) {
     const int m0 = mt * kTM + wm * SH::WM + half * 4;
@@ -394,31 +394,40 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     constexpr int kSc1 = 16;             // cache policy sc1 alone: agent (device) scope
     typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
     int* cnt = g.tile_count + q * (kThreads / 64) + wv;
-    // Sum of the partials of workers wf .. x1 in K order, plus this wavefront's own
-    // accumulators last (own: the owner of the tile's last stage), then the epilogue.
-    auto fixup = [&](int x1, bool own) __attribute__((always_inline)) {
+    // The tile's sum in a fixed order: the part of the owner of the tile's last
+    // stage (worker wl) first, then the partials of workers wf .. wl - 1 in K order;
+    // then the epilogue.  own: this wavefront is that owner and starts from its
+    // accumulators, else it starts from the owner's partial.  Each partial's loads
+    // are issued together, so a partial costs one round trip.
+    auto fixup = [&](bool own) __attribute__((always_inline)) {
 #pragma unroll
       for (int h = 0; h < NCH; ++h) {
         f32x16 v[CT];
-#pragma unroll
-        for (int t = 0; t < CT; ++t) v[t] = f32x16{};
-        for (int x = wf; x <= x1; ++x) {
+        auto load_part = [&](int x, f32x4 (&p4)[CT * 4]) __attribute__((always_inline)) {
           const int off = slot_off(x);
 #pragma unroll
-          for (int t = 0; t < CT; ++t)
-#pragma unroll
-            for (int qd = 0; qd < 4; ++qd) {
-              const f32x4 p4 = __builtin_bit_cast(
-                  f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off + ((h * CT + t) * 4 + qd) * 1024, 0, kSc1));
-#pragma unroll
-              for (int e = 0; e < 4; ++e) v[t][4 * qd + e] += p4[e];
-            }
-        }
+          for (int c = 0; c < CT * 4; ++c)
+            p4[c] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off + (h * CT * 4 + c) * 1024, 0, kSc1));
+        };
         if (own) {
 #pragma unroll
-          for (int t = 0; t < CT; ++t)
+          for (int t = 0; t < CT; ++t) v[t] = acc[(h * CT + t) / J][(h * CT + t) % J];
+        } else {
+          f32x4 p4[CT * 4];
+          load_part(wl, p4);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) v[t][r] += acc[(h * CT + t) / J][(h * CT + t) % J][r];
+          for (int c = 0; c < CT * 4; ++c)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[c >> 2][4 * (c & 3) + e] = p4[c][e];
+        }
+        for (int x = wf; x < wl; ++x) {
+          f32x4 p4[CT * 4];
+          load_part(x, p4);
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int c = 0; c < CT * 4; ++c)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[c >> 2][4 * (c & 3) + e] += p4[c][e];
         }
         epilogue_part(mt, nt, h, v);
       }
@@ -442,7 +451,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
       }
       __atomic_signal_fence(__ATOMIC_SEQ_CST);
       if (seen == wl - wf) {
-        fixup(wl - 1, true);
+        fixup(true);
         return;
       }
     }
@@ -470,7 +479,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     before = __builtin_amdgcn_readfirstlane(before);
     if (before != wl - wf) return;       // not the last to arrive
-    fixup(wl, false);                    // the last to arrive: every part from the partials
+    fixup(false);                        // the last to arrive: every part from the partials
   };
 
   // ---- pipeline: unit u (one K stage of one tile) lives in LDS buffer u % NS.
