@@ -376,6 +376,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
       }
       return;
     }
+    // Only 128-wide tiles are ever cut (the planner deals 256-wide tiles whole), so the
+    // 256-wide instantiations carry no partial protocol (and its registers).
+    if constexpr (TN == 256) return;
     const int q = c.tile - p.dp_tiles;
     const int64_t U = p.sk_units;
     auto owner = [&](int64_t v) __attribute__((always_inline)) { return int(((v + 1) * p.G + U - 1) / U - 1); };
@@ -574,6 +577,8 @@ int finish_polls() {
 
 template <int EPI, int TN>
 void launch_tn(const GemmArgs& g, bool whole_tiles, hipStream_t stream) {
+  static_assert(TN == 128 || TN == 256, "tile width");
+  if (TN == 256) whole_tiles = true;                 // the 256-wide kernels finish whole tiles only
   GemmPlan p{};
   p.m_tiles = cdiv(g.M, kTM);
   p.n_tiles = EPI == kSwiGLU ? g.ffn / (TN / 2) : cdiv(g.N, TN);
