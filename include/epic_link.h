@@ -349,6 +349,12 @@ epic_status epic_link_model(const epic_model_cfg* cfg, const epic_layer_weights*
  * bytes of device memory, 256-byte aligned, owned by the caller; it holds the
  * partial sums of output tiles cut along k and their arrival counters (cleared by
  * this call), so calls in flight at the same time need separate workspaces.
+ * A tile cut along k is summed in a fixed order (the part that holds the tile's last
+ * k stage, then the others in k order), so results do not depend on timing.  The
+ * environment variable EPIC_GEMM_FINISH_POLLS (read at each launch, default 4096)
+ * bounds how long that last part's workgroup polls for the others before falling
+ * back to the last-to-arrive protocol; 0 forces the fallback (a test hook; the sums
+ * are the same either way).
  * Enqueued on `stream` (NULL: the default stream); returns after the enqueue. */
 typedef enum { EPIC_GEMM_STORE = 0, EPIC_GEMM_RESIDUAL = 1, EPIC_GEMM_SWIGLU = 2 } epic_gemm_epilogue;
 size_t epic_gemm_workspace_bytes(void);
