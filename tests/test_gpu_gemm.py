@@ -4,7 +4,8 @@ definitions (oracle.projection, float64 on the bf16 operands).
 Cases: the four projections of the 32-layer link step (736 rows: 256 x 256 and
 256 x 128 tiles cut along K across workgroups), the same projections at a
 compile-sized row count (whole-tile rounds plus cut tiles; checked on sampled
-rows), row and column tails, tiny shapes, and m = 0.  Bars: fp32 outputs
+rows), row and column tails, tiny shapes, tiles cut into up to 56 parts, the
+fallback finish of cut tiles (bit-identical to the polled one), and m = 0.  Bars: fp32 outputs
 max |err| <= 1e-4 * s, s = sqrt(K) * sigma_a * sigma_w (the spread of an output;
 fp32 accumulation of bf16 products leaves ~1e-6 s); SwiGLU (bf16 output)
 |err| <= 2^-8 |ref| + 1e-4 s.
@@ -110,7 +111,21 @@ def test_small_and_ragged(m, n, k, epi):
     _run(m, n, k, epi, tag=20 + SMALL.index((m, n, k, epi)))
 
 
-CUT = [(736, 6144, 4096, "store"), (736, 4096, 14336, "residual"), (300, 1024, 512, "store")]
+MANY = [  # few tiles, long K: a tile cut into 16-56 parts (the last-stage owner waits for all)
+    (64, 128, 14336, "residual"),       # 1 tile, 224 K stages over 56 workgroups
+    (16, 256, 8192, "store"),           # 2 tiles, 32 parts each
+    (1, 128, 4096, "swiglu"),           # one row, one 64-column SwiGLU tile in 16 parts
+    (200, 384, 1024, "swiglu"),         # 3 tiles of 4 parts
+]
+
+
+@pytest.mark.parametrize("m,n,k,epi", MANY, ids=[f"{c[3]}_{c[0]}x{c[1]}x{c[2]}" for c in MANY])
+def test_tiles_cut_into_many_parts(m, n, k, epi):
+    _run(m, n, k, epi, tag=50 + MANY.index((m, n, k, epi)))
+
+
+CUT = [(736, 6144, 4096, "store"), (736, 4096, 14336, "residual"), (300, 1024, 512, "store"),
+       (64, 128, 14336, "residual")]
 
 
 @pytest.mark.parametrize("m,n,k,epi", CUT, ids=[f"{c[3]}_{c[0]}x{c[1]}x{c[2]}" for c in CUT])
