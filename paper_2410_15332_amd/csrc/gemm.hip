@@ -3,7 +3,7 @@
 // A holds the selected rows' activations (bf16, K contiguous), W a weight
 // matrix in [out][in] layout (bf16), so both MFMA operands are read along K.
 // Epilogues are fused:
-//   kStoreF32 : C -> fp32 [M][N]                     (Q/K/V projections, Sec. 4.2)
+//   kStoreF32 : C -> fp32 [M][N]                     (the plain projection of epic_gemm)
 //   kResidual : h[M][N] += C                         (W_O and W_down; fp32 residual stream)
 //   kSwiGLU   : act[M][N/2] = silu(gate) * up, bf16  (W_gate_up; gate rows [0, F), up rows [F, 2F))
 //   kRope     : the fused Q|K|V projection: q and k heads rotated at each row's linked
@@ -29,17 +29,21 @@
 //
 // Scheduling: at most one workgroup per CU (G of them), persistent.  With at least
 // a round of 256 x 256 tiles, whole tiles are dealt in rounds of G, G chosen so the
-// rounds are (nearly) full.  With fewer tiles (short row sets), 256 x 128 tiles are
-// used and the ones that do not fill whole rounds (the last partial round plus one
-// full round, or all of them) are cut along K into G equal shares of K stages, one
-// per workgroup, so every CU gets the same work.
-// A tile cut across workgroups: each wavefront writes its fp32 partial, bumps its
-// arrival counter for the tile, and the last wavefront to arrive sums that part's
-// partials in a fixed order (the result does not depend on arrival order) and runs
-// its epilogue.  Nothing waits for another workgroup.  Workgroups are dealt round-robin to the 8 XCDs; worker indices are
-// arranged so that each XCD works on a contiguous run of tiles, and tiles are
-// ordered in groups of up to 8 row tiles per weight tile, so concurrent workgroups
-// on an XCD share operands through its L2.
+// rounds are (nearly) full; 256-wide tiles are never cut.  With fewer tiles (short
+// row sets), 256 x 128 tiles are used and the ones that do not fill whole rounds
+// (the last partial round plus one full round, or all of them) are cut along K into
+// G equal shares of K stages, one per workgroup, so every CU gets the same work.  A
+// share runs its last segment (the one that starts a tile) first.
+// A tile cut across workgroups: each wavefront part of it has an arrival counter.
+// The owner of the tile's last K stage polls it (a bounded number of times) until
+// the other parts have written their fp32 partials, then adds them to its own
+// accumulators and runs the epilogue; if the polls run out it writes its partial
+// too, and the last wavefront to arrive finishes.  Either way the parts are summed
+// in one fixed order, so the result does not depend on arrival order.  Workgroups
+// are dealt round-robin to the 8 XCDs; worker indices are arranged so that each XCD
+// works on a contiguous run of tiles, and tiles are ordered in groups of up to 8 row
+// tiles per weight tile, so concurrent workgroups on an XCD share operands through
+// its L2.
 // Rows past M and columns past N are computed from clamped rows and never stored.
 #include <algorithm>
 #include <cstdlib>
@@ -262,8 +266,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   // ---- epilogue through buffer descriptors: rows past M fall outside the
   // descriptor's range (loads read 0, stores are dropped).  Accumulator tile
   // t = i*J + j, register r: row wm*WM + i*32 + (r/4)*8 + half*4 + r%4, column
-  // wn*64 + j*32 + col of the workgroup tile.  Written CT tiles (CT / J row blocks)
-  // at a time, so the fixup below never holds more than CT tiles of sums.
+  // wn*64 + j*32 + col of the workgroup tile.  Written CT = 2 tiles (one row block)
+  // at a time, so the fixup below holds two tiles of sums and one partial's two tiles
+  // in flight (with four, the 128-wide kernels ran out of registers and the compiler
+  // reloaded each 1 KB of a partial into the same registers, one round trip each).
   constexpr int NT = I * J, CT = 2, NCH = NT / CT;
   const int col = lane & 31, half = lane >> 5;
   auto epilogue_part = [&](int mt, int nt, int h, const f32x16 (&v)[CT]) __attribute__((always_inline)) {
