@@ -490,7 +490,8 @@ def bench_model(args, wl, n_dummy: int = 0):
     from paper_2410_15332_amd import harness
 
     t0 = time.time()
-    st = harness.stage_model(wl, caches="compile", weights_on_device=True, n_dummy=n_dummy, tile_rows=args.tile_rows)
+    st = harness.stage_model(wl, caches="compile", weights_on_device=True, n_dummy=n_dummy, tile_rows=args.tile_rows,
+                             split_blocks=args.split_blocks)
     torch.cuda.synchronize()
     calibration_copy(args.calibrate_copy_mib)
     log(f"staged {wl.name}: n_s={st.sizes.n_s}, {wl.n_layers} layers, chunks compiled on the GPU "

@@ -224,9 +224,9 @@ class ModelStage:
                            self.v_caches, self.out, self.workspace, stream)
 
 
-def model_cfg(wl, n_layers: int, tile_rows: int = 0) -> el.epic_model_cfg:
-    return el.epic_model_cfg(el.attn_cfg(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, tile_rows=tile_rows), wl.hidden,
-                             wl.ffn, n_layers, wl.rope_theta, wl.rms_eps)
+def model_cfg(wl, n_layers: int, tile_rows: int = 0, split_blocks: int = 0) -> el.epic_model_cfg:
+    return el.epic_model_cfg(el.attn_cfg(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, split_blocks=split_blocks,
+                                         tile_rows=tile_rows), wl.hidden, wl.ffn, n_layers, wl.rope_theta, wl.rms_eps)
 
 
 def _tok_rows(wl, chunk_ids_of_req, chunk_lens, suffix_len, positions, req=0):
@@ -310,7 +310,7 @@ def stage_compile(wl, cfg, layers, final_norm, chunk_blocks, free, num_blocks, n
 def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: float = 0.5, device="cuda",
                 threads: int = 8, weights_on_device: bool = False, n_dummy: int = 0,
                 keep_compile: bool = False, weights: List[Dict[str, object]] = None,
-                rerotate: bool = False, tile_rows: int = 0) -> ModelStage:
+                rerotate: bool = False, tile_rows: int = 0, split_blocks: int = 0) -> ModelStage:
     """Weights, per-chunk caches, link plan and S-row embeddings for a model-level workload.
 
     caches="compile": every chunk is compiled on the GPU by the library itself
@@ -321,13 +321,14 @@ def stage_model(wl, n_layers: int = None, caches: str = "compile", cache_scale: 
     weights: per-layer device tensors from an earlier stage of the same shape, reused.
     rerotate: the link request re-rotates cached K to its linked positions.
     tile_rows: force the attention tile size of the link plan (0: the planner's choice).
+    split_blocks: force the split-KV size of the link plan (0: the planner's choice).
     weights_on_device: draw the weights with a seeded device generator (timing runs)
     instead of synth.model_weights (parity runs).
     """
     import torch
 
     L = n_layers or wl.n_layers
-    cfg = model_cfg(wl, L, tile_rows)
+    cfg = model_cfg(wl, L, tile_rows, split_blocks)
     hq, hkv, d, H = wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.hidden
     acfg = cfg.attn
     given, weights, layers = weights, [], []
