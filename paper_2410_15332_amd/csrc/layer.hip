@@ -35,18 +35,30 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __restrict__ x, const uint16_t* __restrict__ w,
                                                                uint16_t* __restrict__ out_bf16,
                                                                float* __restrict__ out_f32, int hidden, float eps) {
+  // The row stays in registers between the two passes (up to kKeep float4 per
+  // thread, hidden <= 8192 at 256 threads); a longer row is read again.
+  constexpr int kKeep = 8;
   __shared__ float red[kNormThreads / 64];
   const int row = blockIdx.x;
   const float4* xr = reinterpret_cast<const float4*>(x + size_t(row) * hidden);
+  const int n4 = hidden / 4;
+  float4 keep[kKeep];
   float ss = 0.0f;
-  for (int i = threadIdx.x; i < hidden / 4; i += kNormThreads) {
+#pragma unroll
+  for (int k = 0; k < kKeep; ++k) {
+    const int i = threadIdx.x + k * kNormThreads;
+    if (i < n4) {
+      keep[k] = xr[i];
+      ss += keep[k].x * keep[k].x + keep[k].y * keep[k].y + keep[k].z * keep[k].z + keep[k].w * keep[k].w;
+    }
+  }
+  for (int i = threadIdx.x + kKeep * kNormThreads; i < n4; i += kNormThreads) {
     const float4 v = xr[i];
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float total = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(total / float(hidden) + eps);
-  for (int i = threadIdx.x; i < hidden / 4; i += kNormThreads) {
-    const float4 v = xr[i];
+  auto put = [&](int i, const float4& v) {
     const uint2 wb = *reinterpret_cast<const uint2*>(w + 4 * i);
     const float y0 = v.x * inv * bf16_to_f32(uint16_t(wb.x & 0xFFFFu));
     const float y1 = v.y * inv * bf16_to_f32(uint16_t(wb.x >> 16));
@@ -58,7 +70,13 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __re
     } else {
       *reinterpret_cast<float4*>(out_f32 + size_t(row) * hidden + 4 * i) = make_float4(y0, y1, y2, y3);
     }
+  };
+#pragma unroll
+  for (int k = 0; k < kKeep; ++k) {
+    const int i = threadIdx.x + k * kNormThreads;
+    if (i < n4) put(i, keep[k]);
   }
+  for (int i = threadIdx.x + kKeep * kNormThreads; i < n4; i += kNormThreads) put(i, xr[i]);
 }
 
 // cs[row][i] = (cos, sin)(s_pos[row] * theta^(-2i/D)), float64 angle.
