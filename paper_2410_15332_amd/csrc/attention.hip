@@ -281,6 +281,13 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
   // to kLag: the output and the sum share it, so the result is exact, P stays
   // below 2^kLag, and O is rescaled only when some row's max jumps past it.
   constexpr float kLag = 8.0f;
+  // A step of the fast form keeps m if no lane's sum of P passes kFastSum, just
+  // under 2^kLag.  Then no P passed it, so no row maximum rose past m + kLag
+  // (the margin, log2(256 / 255) = 0.0056, covers the roundings of the exponent
+  // and of the full step's test), and the full step would have kept m too:
+  // both forms give the same bits.
+  constexpr float kFastSum = 255.0f;
+  static_assert(kLag == 8.0f, "kFastSum sits just under 2^kLag");
   float m = -INFINITY, lsum = 0.0f;
   const float sl2 = a.scale_log2;
   const int krow = srow_key(col);              // K row this lane feeds into S^T
@@ -338,10 +345,15 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
 
   // One step over tile it.  sc = S(it) on entry (complete); pp = P(it - 1) (PV
   // only); the step leaves P(it) in pc and S(it + 1) in sn (QK only).
-  auto step = [&](auto pv_tag, auto qk_tag, const int it, f32x16 (&sc)[2], f32x16 (&sn)[2],
+  auto step = [&](auto pv_tag, auto qk_tag, auto fast_tag, const int it, f32x16 (&sc)[2], f32x16 (&sn)[2],
                   const u32x4 (&pp)[4], u32x4 (&pc)[4]) __attribute__((always_inline)) {
     constexpr bool PV = decltype(pv_tag)::value;
     constexpr bool QK = decltype(qk_tag)::value;
+    // FAST: an unmasked tile after the first, all scores finite and m finite in
+    // every row; the exponentials use the current m without a row maximum, and
+    // the step is redone as a full one only if some lane's sum of P passes
+    // kFastSum (a row maximum that may have risen past m + kLag).
+    constexpr bool FAST = decltype(fast_tag)::value;
     const int b3 = it % S;                     // buffer of K(it), V(it), K(it + S)
     const int b3n = b3 == S - 1 ? 0 : b3 + 1;  // buffer of K(it + 1) (and V(it + 1) when S = 3)
     const int b3p = b3 == 0 ? S - 1 : b3 - 1;  // buffer of V(it - 1)
@@ -352,7 +364,7 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
 
     // Mask: only tiles past the item's unmasked prefix (diagonal, partial blocks).
     // Register r = i*4 + j of subtile ks holds key ks*32 + (i>>1)*16 + half*8 + (i&1)*4 + j.
-    if (it >= n_fast) {
+    if (!FAST && it >= n_fast) {
       int bpos0[4], blen[4];
 #pragma unroll
       for (int beta = 0; beta < 4; ++beta) {
@@ -378,7 +390,7 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
       kf[1] = kfrag(b3n, 1);
     }
 
-    float mx[4], m_cand = 0.0f, alpha = 1.0f, m_use = 0.0f;
+    float mx[4], m_cand = 0.0f, alpha = 1.0f, m_use = FAST ? m : 0.0f;
     bool grow = false;
     float ps[4];
     // MFMA slots: 0 .. NSLOT-1 the PV product of tile it - 1, NSLOT .. 2 NSLOT-1
@@ -387,18 +399,21 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
     // rescale decision, slots 4.. the exponentials (unit u = score u).
     constexpr int kMaxSlots = 4;
     constexpr int NS2 = 2 * NSLOT;
+    float pe = 0.0f;                           // P of the even unit of the pair being packed
     auto exp_unit = [&](auto uc) __attribute__((always_inline)) {
       constexpr int u = decltype(uc)::value;
       const float p = fast_exp2(__builtin_fmaf(sc[u >> 4][u & 15], sl2, -m_use));
-      sc[u >> 4][u & 15] = p;
       ps[u & 3] = u < 4 ? p : ps[u & 3] + p;
       // Keep this unit's work in its slot: P is only read in the next step and
       // the sums at its end, and the compiler would otherwise move all the
-      // exponentials to those first uses (and hold 32 of them live).
+      // exponentials to those first uses (and hold 32 of them live).  The
+      // scores stay as they are, for the redo of a fast step.
       __asm__ volatile("" ::"v"(ps[u & 3]));
       if constexpr (u & 1) {
-        pc[u >> 3][(u >> 1) & 3] = pack_bf16x2(sc[u >> 4][(u & 15) - 1], p);
+        pc[u >> 3][(u >> 1) & 3] = pack_bf16x2(pe, p);
         __asm__ volatile("" ::"v"(pc[u >> 3][(u >> 1) & 3]));
+      } else {
+        pe = p;
       }
     };
     static_for<NS2>([&](auto qc) __attribute__((always_inline)) {
@@ -425,7 +440,11 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
       }
       // row max over the 32 scores: four chains of three-input maxima (7 + 8 + 8
       // + 8 scores), each step max3(running, a, b), then the chains and the lane swap
-      if constexpr (q == 0) {
+      if constexpr (FAST) {                    // no maximum: one exponential unit per slot share
+        static_for<32>([&](auto uc) __attribute__((always_inline)) {
+          if constexpr ((decltype(uc)::value * NS2) / 32 == q) exp_unit(uc);
+        });
+      } else if constexpr (q == 0) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const int ks = c >> 1, r0 = (c & 1) * 8;
@@ -459,8 +478,37 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
       }
       __builtin_amdgcn_sched_barrier(0);
     });
-    lsum = lsum * alpha + ((ps[0] + ps[1]) + (ps[2] + ps[3]));
-    if (PV && __ballot(grow)) {                // O holds PV(it - 1): move it to the new maximum
+    float ssum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
+    if constexpr (FAST) {
+      if (__ballot(ssum > kFastSum)) {         // redo as the full step: same maximum, same sums
+        float mr = sc[0][0];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mr = fmaxf(mr, sc[ks][r]);
+        m_cand = fmaxf(m, xhalf_max(mr) * sl2);
+        grow = m_cand > m + kLag;
+        alpha = grow ? fast_exp2(m - m_cand) : 1.0f;
+        m = grow ? m_cand : m;
+        m_use = m;
+        static_for<32>([&](auto uc) __attribute__((always_inline)) {
+          constexpr int u = decltype(uc)::value;
+          const float p = fast_exp2(__builtin_fmaf(sc[u >> 4][u & 15], sl2, -m_use));
+          ps[u & 3] = u < 4 ? p : ps[u & 3] + p;
+          if constexpr (u & 1) pc[u >> 3][(u >> 1) & 3] = pack_bf16x2(pe, p);
+          else pe = p;
+        });
+        ssum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
+        if (PV && __ballot(grow)) {
+#pragma unroll
+          for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+        }
+      }
+    }
+    lsum = lsum * alpha + ssum;
+    if (!FAST && PV && __ballot(grow)) {       // O holds PV(it - 1): move it to the new maximum
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -481,23 +529,29 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
   using T = std::true_type;
   using F = std::false_type;
   if (nkv == 1) {
-    step(F{}, F{}, 0, s0, s1, p1, p0);
+    step(F{}, F{}, F{}, 0, s0, s1, p1, p0);
     last_pv(p0, 0);
   } else {
-    step(F{}, T{}, 0, s0, s1, p1, p0);
+    // tile 0 sets m: unmasked (n_fast > 0), it gives every row a finite maximum
+    step(F{}, T{}, F{}, 0, s0, s1, p1, p0);
     int it = 1;
     // two steps per trip while both tiles have a successor; odd tiles keep
-    // their scores / P in s1 / p1, even tiles in s0 / p0
+    // their scores / P in s1 / p1, even tiles in s0 / p0.  Pairs of unmasked
+    // tiles take the fast form.
+    for (; it + 2 < nkv && it + 1 < n_fast; it += 2) {
+      step(T{}, T{}, T{}, it, s1, s0, p0, p1);
+      step(T{}, T{}, T{}, it + 1, s0, s1, p1, p0);
+    }
     for (; it + 2 < nkv; it += 2) {
-      step(T{}, T{}, it, s1, s0, p0, p1);
-      step(T{}, T{}, it + 1, s0, s1, p1, p0);
+      step(T{}, T{}, F{}, it, s1, s0, p0, p1);
+      step(T{}, T{}, F{}, it + 1, s0, s1, p1, p0);
     }
     if (it + 1 < nkv) {                        // tiles it (odd) and it + 1 (last) remain
-      step(T{}, T{}, it, s1, s0, p0, p1);
-      step(T{}, F{}, it + 1, s0, s1, p1, p0);
+      step(T{}, T{}, F{}, it, s1, s0, p0, p1);
+      step(T{}, F{}, F{}, it + 1, s0, s1, p1, p0);
       last_pv(p0, (it + 1) % S);
     } else {                                   // tile it (odd) is the last
-      step(T{}, F{}, it, s1, s0, p0, p1);
+      step(T{}, F{}, F{}, it, s1, s0, p0, p1);
       last_pv(p1, it % S);
     }
   }
