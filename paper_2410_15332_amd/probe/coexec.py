@@ -1,14 +1,19 @@
 """Run the co-execution probe (coexec.hip in the probe library) and print, per
 variant, the shader cycles per iteration of 8 MFMA slots and the engine clock.
+Modes: accumulators in AGPRs or VGPRs, and 4, 2 or 1 independent accumulator chains.
 
     python -m paper_2410_15332_amd.probe.coexec
 """
 import ctypes
 import os
 
-VARIANTS = [(1, 0, 0), (0, 32, 0), (0, 32, 1), (0, 32, 2), (1, 16, 0), (1, 32, 0), (1, 48, 0), (1, 64, 0),
-            (1, 16, 1), (1, 32, 1), (1, 48, 1)]
+VARIANTS = [(1, 0, 0), (0, 32, 0), (0, 32, 1), (0, 32, 2),
+            (1, 16, 0), (1, 32, 0), (1, 48, 0), (1, 64, 0), (1, 8, 1), (1, 16, 1), (1, 32, 1), (1, 16, 2), (1, 32, 2),
+            (2, 0, 0), (2, 32, 0), (2, 48, 0), (2, 16, 1), (2, 32, 1),
+            (3, 0, 0), (3, 32, 0), (4, 0, 0), (4, 32, 0)]
 KINDS = {0: "fma", 1: "exp", 2: "max"}
+MODES = {0: "no mfma              ", 1: "8 mfma (AGPR acc, 4) ", 2: "8 mfma (VGPR acc, 4) ",
+         3: "8 mfma (AGPR acc, 2) ", 4: "8 mfma (AGPR acc, 1) "}
 
 
 def main():
@@ -32,7 +37,7 @@ def main():
             torch.cuda.synchronize()
             c = cyc.view(-1, 2).double()
             cycles, ticks = c[:, 0].mean().item(), c[:, 1].mean().item()
-            label = f"{'8 mfma +' if mfma else 'no mfma '} {nv:2d} {KINDS[kind]}"
+            label = f"{MODES[mfma]}+ {nv:2d} {KINDS[kind]}"
             print(f"{label}  waves/SIMD={per_simd}: {cycles / iters:7.1f} cycles/iter "
                   f"({cycles / iters / 8:5.1f} per MFMA slot)  clock {cycles / (ticks * 10.0):.2f} GHz", flush=True)
 
