@@ -287,6 +287,7 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
   // and of the full step's test), and the full step would have kept m too:
   // both forms give the same bits.
   constexpr float kFastSum = 255.0f;
+  constexpr int kFastMin = 16;                 // unmasked tiles an item needs to take the fast form
   static_assert(kLag == 8.0f, "kFastSum sits just under 2^kLag");
   float m = -INFINITY, lsum = 0.0f;
   const float sl2 = a.scale_log2;
@@ -538,7 +539,7 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
     // two steps per trip while both tiles have a successor; odd tiles keep
     // their scores / P in s1 / p1, even tiles in s0 / p0.  Pairs of unmasked
     // tiles take the fast form.
-    for (; it + 2 < nkv && it + 1 < n_fast; it += 2) {
+    for (; n_fast >= kFastMin && it + 2 < nkv && it + 1 < n_fast; it += 2) {
       step(T{}, T{}, T{}, it, s1, s0, p0, p1);
       step(T{}, T{}, T{}, it + 1, s0, s1, p1, p0);
     }
