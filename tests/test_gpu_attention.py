@@ -215,6 +215,32 @@ def test_edge_cases(wl, tile_rows):
 
 
 @pytest.mark.parametrize("tile_rows", TILE_ROWS)
+def test_fast_step_redo(tile_rows):
+    """Long unmasked prefixes (the fast step form, no row maximum) under large logits
+    (q and k ~ N(0, 5)), so that row maxima jump by more than 2^8 in P after the first
+    tile and the fast step is redone as the full one.  No split: every item starts at
+    key 0 with 32 or more unmasked 64-key tiles.  V ~ N(0, 0.25) keeps the outputs near
+    1 in size: the rows are nearly one-hot, and with V ~ N(0, 1) an output of 4.19
+    lands one bf16 step (0.031 there) from the reference, 0.030, with the same bits as
+    the kernel without the fast form (bf16 P under a lagging maximum: 2^-9 relative)."""
+    wl = _wl("fast_redo", [2048, 2048, 1024], [[0, 1, 2]], [33], 32, 32, 8, 128, scale=0.25, qk_scale=20.0)
+    # The case must reach the redo: some (row, head) of chunk 1 (all of chunks 0..1
+    # visible) has a logit past its first 64 keys that is more than 8 (log2 units)
+    # above the maximum over those keys.
+    lens = wl.chunk_lens[:3]
+    s_pos = oracle.legolink_positions(lens, wl.suffix_lens[0], wl.k)
+    kc = _f64(synth.chunk_cache(wl.seed, 0, 2048, 8, 128, wl.value_scale, qk_scale=wl.qk_scale)[0])
+    q = _f64(synth.row_qkv(wl.seed, 0, s_pos[:32], 32, 8, 128, wl.value_scale, wl.qk_scale)[0])
+    lg = np.einsum("rhd,khd->rhk", q, np.repeat(kc, 4, axis=1)) / np.sqrt(128.0) * np.log2(np.e)
+    jump = lg[:, :, 64:].max(axis=2) - lg[:, :, :64].max(axis=2)
+    assert (jump > 8.0).sum() > 0, "case does not exercise the fast step's redo"
+    st = _stage(wl, split_blocks=1 << 20, tile_rows=tile_rows)
+    assert st.sizes.tile_rows == tile_rows and st.sizes.n_partials == 0
+    st.run()
+    check_stage(st)
+
+
+@pytest.mark.parametrize("tile_rows", TILE_ROWS)
 @pytest.mark.parametrize("split", [4, 8, 36])
 def test_forced_split_kv(split, tile_rows):
     """Small split sizes: most rows merge many partials in the combine kernel."""
