@@ -32,8 +32,9 @@
 //
 // Software pipeline: step i issues the PV product of tile i-1 and the QK
 // product of tile i+1, alternating, and spreads the softmax of tile i (row
-// maximum, then the 32 exponentials per lane) over those 32 MFMAs, so the
-// matrix cores always have independent work beside the vector ALU work.
+// maximum, then the 32 exponentials per lane) and the step's buffer->LDS loads
+// over those 32 MFMAs, so the matrix cores always have independent work beside
+// the vector ALU work.
 #include <utility>
 
 #include "device_common.h"
@@ -88,6 +89,13 @@ __device__ __forceinline__ void dma_block(__amdgpu_buffer_rsrc_t rs, char* dst, 
                                             GOFF::template at<I>(), 0),
    ...);
 #endif
+}
+// One 16-byte-per-lane buffer->LDS load (lane l's 16 bytes land at dst + 16 l, the
+// lane offset moving the memory address only).  A plain function, so that a call
+// from a kernel template is never a template-dependent expression (the host pass
+// cannot check the builtin there and would drop the kernel).
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, char* dst, int voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)dst, 16, voff, 0, 0, 0);
 }
 // K load I of a D-wide block: row group rb = 64 I / (8 NCH), chunk base v0 = (64 I % (8 NCH)) / 8;
 // lane l reads row 8 rb + l % 8, chunk (v0 + l / 8) ^ rb.
@@ -230,6 +238,26 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
     dma_block<VLoads>(rs, reinterpret_cast<char*>(&lds.v[buf][dw * D * 16]), vvo, vvo,
                       std::make_integer_sequence<int, NI>{});
   };
+  // The same loads one at a time (load I of the block), from a descriptor made once.
+  auto rsrc_k = [&](int phys) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(kbase) + size_t(phys) * blk_bytes, 0, 16 * D * 2,
+                                             kBufWord3);
+  };
+  auto rsrc_v = [&](int phys) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(vbase) + size_t(phys) * blk_bytes, 0, 16 * D * 2,
+                                             kBufWord3);
+  };
+  // W = 8: a wavefront loads K or V, so one pair of lane offsets serves either
+  const int so_even = W == 8 && !k_wave ? vvo : kvo;
+  const int so_odd = W == 8 && !k_wave ? vvo : kvo ^ 16;
+  auto dma_k1 = [&](auto ic, int buf, __amdgpu_buffer_rsrc_t rs) __attribute__((always_inline)) {
+    dma_block<KLoads<D>>(rs, reinterpret_cast<char*>(&lds.k[buf][16 * dw * D]), W == 8 ? so_even : kvo,
+                         W == 8 ? so_odd : kvo ^ 16, std::integer_sequence<int, decltype(ic)::value>{});
+  };
+  auto dma_v1 = [&](auto ic, int buf, __amdgpu_buffer_rsrc_t rs) __attribute__((always_inline)) {
+    dma_block<VLoads>(rs, reinterpret_cast<char*>(&lds.v[buf][dw * D * 16]), W == 8 ? so_even : vvo,
+                      W == 8 ? so_even : vvo, std::integer_sequence<int, decltype(ic)::value>{});
+  };
 
   // Block metadata, read with scalar loads: the tables are read-only while the
   // kernel runs, and scalar loads are counted by lgkmcnt, so waiting for them
@@ -358,8 +386,18 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
     const int b3 = it % S;                     // buffer of K(it), V(it), K(it + S)
     const int b3n = b3 == S - 1 ? 0 : b3 + 1;  // buffer of K(it + 1) (and V(it + 1) when S = 3)
     const int b3p = b3 == 0 ? S - 1 : b3 - 1;  // buffer of V(it - 1)
-    if (k_wave) dma_k(b3, pk);                                 // K(it + S): its buffer held K(it)
-    if (v_wave) dma_v(S == 3 ? b3n : b3, pv);                  // V(it + S - 2): its buffer held V(it - 2)
+    // K(it + S) into b3 (its buffer held K(it)) and V(it + S - 2) into the buffer of
+    // V(it - 2): both buffers are free for the whole step, so the step's loads are
+    // spread over its MFMA slots rather than issued together after the barrier, where
+    // the eight wavefronts' loads queued behind each other.  W = 8: load I at slot
+    // I * KSP + (I odd ? KSP / 2 : 0).  W = 4: K load I at slot I * KSP, V load I half
+    // a spacing later, all within the first half of the step (S = 2: the loads must
+    // land by the step's end).
+    const auto rk = rsrc_k(pk);
+    const auto rv = rsrc_v(pv);
+    const int vbuf = S == 3 ? b3n : b3;
+    char* const dma_dst = k_wave ? reinterpret_cast<char*>(&lds.k[b3][16 * dw * D])
+                                 : reinterpret_cast<char*>(&lds.v[vbuf][dw * D * 16]);
     const int pk_next = k_wave ? phys_k(it + 1) : 0;
     const int pv_next = v_wave ? phys_v(it + 1) : 0;
 
@@ -419,6 +457,23 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
     };
     static_for<NS2>([&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
+      constexpr int KSP = (S == 3 ? NS2 : NS2 / 2) / NI;     // slots between a wavefront's K loads
+      static_for<NI>([&](auto ic) __attribute__((always_inline)) {
+        constexpr int I = decltype(ic)::value;
+        if constexpr (W == 8) {
+          // one load per wavefront and slot, K or V by uniform selects (no branch
+          // among the MFMAs); the K / V offset of load I rides in the lane offset,
+          // which moves the memory address only
+          if constexpr (q == I * KSP + (I & 1) * (KSP / 2)) {
+            const int voff = (KLoads<D>::template odd<I>() ? so_odd : so_even) +
+                             (k_wave ? KLoads<D>::template at<I>() : VLoads::template at<I>());
+            dma16(k_wave ? rk : rv, dma_dst + 1024 * I, voff);
+          }
+        } else {
+          if constexpr (q == I * KSP) dma_k1(ic, b3, rk);
+          if constexpr (q == I * KSP + KSP / 2) dma_v1(ic, vbuf, rv);
+        }
+      });
       if constexpr (q + 2 < NSLOT) {
         if constexpr (PV) vf[(q + 2) % 3] = vfrag(b3p, q + 2);
       } else if constexpr (q + 2 < NS2) {
