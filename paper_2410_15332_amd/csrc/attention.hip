@@ -271,6 +271,17 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
   // physical ids this wavefront stages in step ts: K(ts + S) and V(ts + S - 2), block dw
   auto phys_k = [&](int ts) -> int { return blk_at(lb_c, b0 + 4 * (ts + S) + dw); };
   auto phys_v = [&](int ts) -> int { return blk_at(lb_c, b0 + 4 * (ts + S - 2) + dw); };
+  // W = 8 reads the ids of later steps ahead with a vector load (every lane loads
+  // the same word), two steps before their use: a scalar load in the step waited
+  // for its reply at once (an LDS wait behind a scalar load must be a full wait,
+  // since scalar loads may return out of order), several hundred cycles a step.
+  // Vector loads complete in issue order with the buffer->LDS loads, so the step's
+  // closing wait covers them.  The index is clamped into [b0, b1) as above.
+  const auto lb_rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.linked_blocks), 0, b1 * 4, kBufWord3);
+  auto id_index = [&](int ts) -> int {
+    return max(b0, min(b0 + 4 * (ts + (k_wave ? S : S - 2)) + dw, b1 - 1));
+  };
+  int idr[2] = {0, 0};                         // ids of steps of either parity, in flight (W = 8)
   // first position / valid slots of block beta of tile ts (0 slots past b1)
   auto blk_pos = [&](int ts, int beta) -> int { return blk_at(pos_c, b0 + 4 * ts + beta); };
   auto blk_len = [&](int ts, int beta) -> int {
@@ -359,6 +370,7 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
     for (int j = 0; j < S - 2; ++j) dma_v(j, phys_v(j - S + 2));
   }
   int pk = phys_k(0), pv = phys_v(0);          // blocks this wavefront stages in the current step
+  if constexpr (W == 8) idr[1] = __builtin_amdgcn_raw_buffer_load_b32(lb_rs, 0, id_index(1) * 4, 0);
   wait_vmem<0>();
   if (S == 3 && v_wave) fix_v(0, 0, blk_len(0, dw));
   __syncthreads();
@@ -374,10 +386,11 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
 
   // One step over tile it.  sc = S(it) on entry (complete); pp = P(it - 1) (PV
   // only); the step leaves P(it) in pc and S(it + 1) in sn (QK only).
-  auto step = [&](auto pv_tag, auto qk_tag, auto fast_tag, const int it, f32x16 (&sc)[2], f32x16 (&sn)[2],
-                  const u32x4 (&pp)[4], u32x4 (&pc)[4]) __attribute__((always_inline)) {
+  auto step = [&](auto pv_tag, auto qk_tag, auto fast_tag, auto par_tag, const int it, f32x16 (&sc)[2],
+                  f32x16 (&sn)[2], const u32x4 (&pp)[4], u32x4 (&pc)[4]) __attribute__((always_inline)) {
     constexpr bool PV = decltype(pv_tag)::value;
     constexpr bool QK = decltype(qk_tag)::value;
+    constexpr int PAR = decltype(par_tag)::value;   // it % 2
     // FAST: an unmasked tile after the first, all scores finite and m finite in
     // every row; the exponentials use the current m without a row maximum, and
     // the step is redone as a full one only if some lane's sum of P passes
@@ -398,8 +411,11 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
     const int vbuf = S == 3 ? b3n : b3;
     char* const dma_dst = k_wave ? reinterpret_cast<char*>(&lds.k[b3][16 * dw * D])
                                  : reinterpret_cast<char*>(&lds.v[vbuf][dw * D * 16]);
-    const int pk_next = k_wave ? phys_k(it + 1) : 0;
-    const int pv_next = v_wave ? phys_v(it + 1) : 0;
+    int pk_next = 0, pv_next = 0;
+    if constexpr (W == 4) {
+      pk_next = phys_k(it + 1);
+      pv_next = phys_v(it + 1);
+    }
 
     // Mask: only tiles past the item's unmasked prefix (diagonal, partial blocks).
     // Register r = i*4 + j of subtile ks holds key ks*32 + (i>>1)*16 + half*8 + (i&1)*4 + j.
@@ -458,6 +474,10 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
     static_for<NS2>([&](auto qc) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
       constexpr int KSP = (S == 3 ? NS2 : NS2 / 2) / NI;     // slots between a wavefront's K loads
+      if constexpr (W == 8 && q == 1) {
+        // id of step it + 2 (same parity), after this step's first buffer->LDS load
+        idr[PAR] = __builtin_amdgcn_raw_buffer_load_b32(lb_rs, 0, id_index(it + 2) * 4, 0);
+      }
       static_for<NI>([&](auto ic) __attribute__((always_inline)) {
         constexpr int I = decltype(ic)::value;
         if constexpr (W == 8) {
@@ -570,11 +590,18 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
     }
-    wait_vmem<S == 3 ? NI : 0>();              // this wavefront's loads of K(it + 2), V(it)
+    // this wavefront's loads of K(it + 2), V(it) (W = 8: and the id of step it + 1)
+    wait_vmem<S == 3 ? NI + 1 : 0>();
     if (v_wave) fix_v(b3, it, blk_len(it, dw));
     barrier_lds();                             // ... of every wavefront: visible, buffers free
-    pk = pk_next;
-    pv = pv_next;
+    if constexpr (W == 8) {
+      const int id = __builtin_amdgcn_readfirstlane(idr[PAR ^ 1]);
+      pk = id;
+      pv = id;
+    } else {
+      pk = pk_next;
+      pv = pv_next;
+    }
   };
   // PV of the last tile (nothing left to overlap it with).
   auto last_pv = [&](const u32x4 (&pp)[4], int buf) __attribute__((always_inline)) {
@@ -584,30 +611,32 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
 
   using T = std::true_type;
   using F = std::false_type;
+  using E = std::integral_constant<int, 0>;   // even step
+  using O = std::integral_constant<int, 1>;   // odd step
   if (nkv == 1) {
-    step(F{}, F{}, F{}, 0, s0, s1, p1, p0);
+    step(F{}, F{}, F{}, E{}, 0, s0, s1, p1, p0);
     last_pv(p0, 0);
   } else {
     // tile 0 sets m: unmasked (n_fast > 0), it gives every row a finite maximum
-    step(F{}, T{}, F{}, 0, s0, s1, p1, p0);
+    step(F{}, T{}, F{}, E{}, 0, s0, s1, p1, p0);
     int it = 1;
     // two steps per trip while both tiles have a successor; odd tiles keep
     // their scores / P in s1 / p1, even tiles in s0 / p0.  Pairs of unmasked
     // tiles take the fast form.
     for (; n_fast >= kFastMin && it + 2 < nkv && it + 1 < n_fast; it += 2) {
-      step(T{}, T{}, T{}, it, s1, s0, p0, p1);
-      step(T{}, T{}, T{}, it + 1, s0, s1, p1, p0);
+      step(T{}, T{}, T{}, O{}, it, s1, s0, p0, p1);
+      step(T{}, T{}, T{}, E{}, it + 1, s0, s1, p1, p0);
     }
     for (; it + 2 < nkv; it += 2) {
-      step(T{}, T{}, F{}, it, s1, s0, p0, p1);
-      step(T{}, T{}, F{}, it + 1, s0, s1, p1, p0);
+      step(T{}, T{}, F{}, O{}, it, s1, s0, p0, p1);
+      step(T{}, T{}, F{}, E{}, it + 1, s0, s1, p1, p0);
     }
     if (it + 1 < nkv) {                        // tiles it (odd) and it + 1 (last) remain
-      step(T{}, T{}, F{}, it, s1, s0, p0, p1);
-      step(T{}, F{}, F{}, it + 1, s0, s1, p1, p0);
+      step(T{}, T{}, F{}, O{}, it, s1, s0, p0, p1);
+      step(T{}, F{}, F{}, E{}, it + 1, s0, s1, p1, p0);
       last_pv(p0, (it + 1) % S);
     } else {                                   // tile it (odd) is the last
-      step(T{}, F{}, F{}, it, s1, s0, p0, p1);
+      step(T{}, F{}, F{}, O{}, it, s1, s0, p0, p1);
       last_pv(p1, it % S);
     }
   }
