@@ -247,17 +247,17 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(vbase) + size_t(phys) * blk_bytes, 0, 16 * D * 2,
                                              kBufWord3);
   };
-  // W = 8: a wavefront loads K or V, so one pair of lane offsets serves either
-  const int so_even = W == 8 && !k_wave ? vvo : kvo;
-  const int so_odd = W == 8 && !k_wave ? vvo : kvo ^ 16;
   auto dma_k1 = [&](auto ic, int buf, __amdgpu_buffer_rsrc_t rs) __attribute__((always_inline)) {
-    dma_block<KLoads<D>>(rs, reinterpret_cast<char*>(&lds.k[buf][16 * dw * D]), W == 8 ? so_even : kvo,
-                         W == 8 ? so_odd : kvo ^ 16, std::integer_sequence<int, decltype(ic)::value>{});
+    dma_block<KLoads<D>>(rs, reinterpret_cast<char*>(&lds.k[buf][16 * dw * D]), kvo, kvo ^ 16,
+                         std::integer_sequence<int, decltype(ic)::value>{});
   };
   auto dma_v1 = [&](auto ic, int buf, __amdgpu_buffer_rsrc_t rs) __attribute__((always_inline)) {
-    dma_block<VLoads>(rs, reinterpret_cast<char*>(&lds.v[buf][dw * D * 16]), W == 8 ? so_even : vvo,
-                      W == 8 ? so_even : vvo, std::integer_sequence<int, decltype(ic)::value>{});
+    dma_block<VLoads>(rs, reinterpret_cast<char*>(&lds.v[buf][dw * D * 16]), vvo, vvo,
+                      std::integer_sequence<int, decltype(ic)::value>{});
   };
+  // W = 8: a wavefront loads K or V, so one pair of lane offsets serves either
+  const int so_even = !k_wave ? vvo : kvo;
+  const int so_odd = !k_wave ? vvo : kvo ^ 16;
 
   // Block metadata, read with scalar loads: the tables are read-only while the
   // kernel runs, and scalar loads are counted by lgkmcnt, so waiting for them
@@ -272,11 +272,11 @@ __global__ __launch_bounds__(64 * W, W == 8 ? 1 : 2) void link_attention_kernel(
   auto phys_k = [&](int ts) -> int { return blk_at(lb_c, b0 + 4 * (ts + S) + dw); };
   auto phys_v = [&](int ts) -> int { return blk_at(lb_c, b0 + 4 * (ts + S - 2) + dw); };
   // W = 8 reads the ids of later steps ahead with a vector load (every lane loads
-  // the same word), two steps before their use: a scalar load in the step waited
-  // for its reply at once (an LDS wait behind a scalar load must be a full wait,
-  // since scalar loads may return out of order), several hundred cycles a step.
-  // Vector loads complete in issue order with the buffer->LDS loads, so the step's
-  // closing wait covers them.  The index is clamped into [b0, b1) as above.
+  // the same word), two steps before their use: a scalar load in the step had its
+  // reply waited for at once (an LDS wait behind a scalar load must be a full wait,
+  // since scalar loads may return out of order).  Vector loads complete in issue
+  // order with the buffer->LDS loads, so the step's closing wait covers them.  The
+  // index is clamped into [b0, b1) as above.
   const auto lb_rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.linked_blocks), 0, b1 * 4, kBufWord3);
   auto id_index = [&](int ts) -> int {
     return max(b0, min(b0 + 4 * (ts + (k_wave ? S : S - 2)) + dw, b1 - 1));
