@@ -262,6 +262,21 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
 #pragma unroll
       for (int j = 0; j < J; ++j) acc[i][j] = mfma_32x32x16(f.a[i], f.b[j], acc[i][j]);
   };
+  // mma(f) with the loads of unit kt into buffer buf between its MFMAs (NLA / (I J)
+  // after each, same MFMA order as mma): issued together after the barrier, the
+  // workgroup's 64 loads of 1 KB queued behind each other while no MFMA was issued.
+  auto mma_dma = [&](const Frags& f, int buf, int kt) __attribute__((always_inline)) {
+    constexpr int NM = I * J;
+    char* const dst = dma_base + buf * dma_stage;
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      acc[m / J][m % J] = mfma_32x32x16(f.a[m / J], f.b[m % J], acc[m / J][m % J]);
+#pragma unroll
+      for (int i = m * NLA / NM; i < (m + 1) * NLA / NM; ++i)
+        if (!dma_idle && (i < SH::NLB || a_wave)) dma16(rs, dst + i * 1024, vo[i], kt * (kBK * 2));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
 
   // ---- epilogue through buffer descriptors: rows past M fall outside the
   // descriptor's range (loads read 0, stores are dropped).  Accumulator tile
@@ -503,13 +518,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   dc = cc;
   int dtile = dc.tile;
   dma_setup(dtile);
-  auto dma_next = [&](int buf) __attribute__((always_inline)) {
-    dma(buf, dc.kt);
+  auto dma_advance = [&]() __attribute__((always_inline)) {
     advance(dc);
     if (dc.tile != dtile) {
       dtile = dc.tile;
       dma_setup(dtile);
     }
+  };
+  auto dma_next = [&](int buf) __attribute__((always_inline)) {
+    dma(buf, dc.kt);
+    dma_advance();
   };
 #pragma unroll
   for (int b = 0; b < NS; ++b) dma_next(b);
@@ -545,11 +563,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
       if (a_wave) wait_vmem<(NS - 2) * NLA>();  // this wavefront's loads of unit u + 1
       else wait_vmem<(NS - 2) * SH::NLB>();
       barrier_lds();
-      dma_next(buf);
       if (live) {
         read(f0, nbuf, 0);
-        mma(f1);
+        mma_dma(f1, buf, dc.kt);                  // unit u + NS into buf, between the MFMAs
+      } else {
+        dma(buf, dc.kt);
       }
+      dma_advance();
       buf = nbuf;
     }
     finish(cc);
