@@ -9,11 +9,11 @@
 //   kRope     : the fused Q|K|V projection: q and k heads rotated at each row's linked
 //               position (rotary pairs (i, i + D/2)), v heads as they are; bf16 q, k, v
 //
-// Tiling: workgroup tile 256 x TN, 8 wavefronts of 64 columns each (TN = 256:
-// 2 x 4 wavefronts of 128 x 64, i.e. 4 x 2 v_mfma_f32_32x32x16_bf16 tiles; TN = 128:
-// 4 x 2 wavefronts of 64 x 64).  K runs in stages of 64 staged in LDS by direct
-// buffer->LDS loads, NS stages in LDS (2 at TN = 256, 3 at TN = 128; loads issued
-// NS - 1 stages ahead of use).  An operand stage is groups of 8 rows of 128 bytes
+// Tiling: workgroup tile TM x TN (256 x 256, 192 x 256 or 256 x 128), 8 wavefronts of
+// 64 columns each (TN = 256: 2 x 4 wavefronts of TM/2 x 64, i.e. 4 x 2 or 3 x 2
+// v_mfma_f32_32x32x16_bf16 tiles; TN = 128: 4 x 2 wavefronts of 64 x 64).  K runs
+// in stages of 64 staged in LDS by direct buffer->LDS loads, NS stages in LDS (2 at
+// TN = 256, 3 at TN = 128; loads issued NS - 1 stages ahead of use).  An operand stage is groups of 8 rows of 128 bytes
 // (one whole cache line per row: a load instruction that covers 16 half lines moves
 // about 0.6x the bytes per cycle of one that covers 8 whole lines); row r sits at byte
 // 128 r with its eight 16-byte chunks XOR-swizzled by (r / 2) % 8, so one load
@@ -28,8 +28,8 @@
 // columns ip and ip + 64.
 //
 // Scheduling: at most one workgroup per CU (G of them), persistent.  With at least
-// a round of 256 x 256 tiles, whole tiles are dealt in rounds of G, G chosen so the
-// rounds are (nearly) full; 256-wide tiles are never cut.  With fewer tiles (short
+// a round of 256 x 256 tiles, whole 256-wide tiles (256 or 192 rows) are dealt in
+// rounds of G, G chosen so the rounds are (nearly) full; 256-wide tiles are never cut.  With fewer tiles (short
 // row sets), 256 x 128 tiles are used and the ones that do not fill whole rounds
 // (the last partial round plus one full round, or all of them) are cut along K into
 // G equal shares of K stages, one per workgroup, so every CU gets the same work.  A
@@ -64,17 +64,19 @@ constexpr int kMaxSplitTiles = 2 * kMaxWorkers;
 constexpr int kCounters = kMaxSplitTiles * (kThreads / 64);   // one per (cut tile, wavefront)
 constexpr int kMinUnits = 4;                            // K stages per workgroup, at least
 
-template <int TN>
+template <int TM, int TN>
 struct Shape {
-  static constexpr int NS = TN == 256 ? 2 : 3;          // LDS stages (128 / 144 KB)
+  static_assert((TM == 256 && (TN == 128 || TN == 256)) || (TM == 192 && TN == 256), "tile shape");
+  static constexpr int NS = TN == 256 ? 2 : 3;          // LDS stages (128 / 112 / 144 KB)
   static constexpr int WAVES_M = TN == 256 ? 2 : 4;     // wavefronts along M
-  static constexpr int WM = kTM / WAVES_M;              // rows per wavefront
+  static constexpr int WM = TM / WAVES_M;               // rows per wavefront
   static constexpr int I = WM / 32;                     // 32-row MFMA tiles per wavefront
   static constexpr int J = 2;                           // 32-column MFMA tiles per wavefront
-  static constexpr int A_STAGE = kTM * kBK * 2;         // bytes per stage
+  static constexpr int A_STAGE = TM * kBK * 2;          // bytes per stage
   static constexpr int B_STAGE = TN * kBK * 2;
-  static constexpr int NLA = kTM / 32;                  // A row groups (8 rows) per loading wavefront
+  static constexpr int NLA = TM / 32;                   // A row groups (8 rows) per loading wavefront
   static constexpr int NLB = TN / 32;                   // W row groups per loading wavefront
+  static constexpr int NL = NLA > NLB ? NLA : NLB;
 };
 
 struct GemmPlan {
@@ -86,10 +88,10 @@ struct GemmPlan {
   int polls;                   // counter polls of a cut tile's last-stage owner before it falls back
 };
 
-template <int TN>
+template <int TM, int TN>
 struct GemmLds {
-  char a[Shape<TN>::NS][Shape<TN>::A_STAGE];
-  char b[Shape<TN>::NS][Shape<TN>::B_STAGE];
+  char a[Shape<TM, TN>::NS][Shape<TM, TN>::A_STAGE];
+  char b[Shape<TM, TN>::NS][Shape<TM, TN>::B_STAGE];
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -120,11 +122,11 @@ struct Cursor {
   int u, tile, kt, kbeg, kend;
 };
 
-template <int EPI, int TN>
+template <int EPI, int TM, int TN>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan p) {
-  using SH = Shape<TN>;
-  constexpr int NS = SH::NS, I = SH::I, J = SH::J, NLA = SH::NLA;
-  __shared__ __attribute__((aligned(1024))) GemmLds<TN> lds;
+  using SH = Shape<TM, TN>;
+  constexpr int NS = SH::NS, I = SH::I, J = SH::J, NLA = SH::NLA, NLB = SH::NLB, NL = SH::NL;
+  __shared__ __attribute__((aligned(1024))) GemmLds<TM, TN> lds;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -179,29 +181,32 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     if (++c.kt == c.kend) seek(c, c.u);
   };
 
-  // ---- buffer->LDS loads: wavefronts 0..3 stage the 32 A row groups (8 each),
+  // ---- buffer->LDS loads: wavefronts 0..3 stage the TM / 8 A row groups (NLA each),
   // 4..7 the TN / 8 W row groups (NLB each).
   const bool a_wave = wv < 4;
   // With M <= 128 (one row tile) the A row groups 16..31 hold no row of A: their
   // loading wavefronts issue nothing (none of their waits then has anything to wait for).
   const bool dma_idle = TN == 128 && a_wave && g.M <= 128 && wv >= 2;
-  const int nl = a_wave ? NLA : SH::NLB;               // loads per stage of this wavefront
+  const int nl = a_wave ? NLA : NLB;                   // loads per stage of this wavefront
   const int grp0 = nl * (wv & 3);
   const int lrow = lane >> 3;                              // row within an 8-row group
   const int row_bytes = g.K * 2;
   const int w_rows = EPI == kSwiGLU ? 2 * g.ffn : g.N;
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a_wave ? g.A : g.W), 0, (a_wave ? g.M : w_rows) * row_bytes, kBufWord3);
-  int vo[kTM / 32];                                     // lane byte offsets of the row groups (NLA)
+  int vo[NL];                                           // lane byte offsets of the row groups (nl)
+  // load i of a stage: issued by this wavefront (i < nl; the bound is a constant for
+  // the i below both counts)
+  auto has_load = [&](int i) __attribute__((always_inline)) { return a_wave ? i < NLA : i < NLB; };
   auto dma_setup = [&](int tile) __attribute__((always_inline)) {
     int mt, nt;
     tile_mn(tile, mt, nt);
 #pragma unroll
-    for (int i = 0; i < NLA; ++i) {
+    for (int i = 0; i < NL; ++i) {
       const int row = (grp0 + i) * 8 + lrow;               // row of the operand tile
       const int lchunk = (lane & 7) ^ ((row >> 1) & 7);    // 16-byte chunk of that row this lane loads
       int gr;
-      if (a_wave) gr = min(mt * kTM + row, g.M - 1);
+      if (a_wave) gr = min(mt * TM + row, g.M - 1);
       else if constexpr (EPI == kSwiGLU)
         gr = ((row >> 5) & 1) * g.ffn + nt * (TN / 2) + (row >> 6) * 32 + (row & 31);
       else if constexpr (EPI == kRope) {
@@ -220,9 +225,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     if (dma_idle) return;
     char* dst = dma_base + buf * dma_stage;
 #pragma unroll
-    for (int i = 0; i < NLA; ++i)
-      if (i < SH::NLB || a_wave)
-        dma16(rs, dst + i * 1024, vo[i], kt * (kBK * 2));
+    for (int i = 0; i < NL; ++i)
+      if (has_load(i)) dma16(rs, dst + i * 1024, vo[i], kt * (kBK * 2));
   };
 
   // ---- MFMA operands: for k-slice ks (16 wide, 4 per stage) lane l reads row l % 32
@@ -262,7 +266,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
 #pragma unroll
       for (int j = 0; j < J; ++j) acc[i][j] = mfma_32x32x16(f.a[i], f.b[j], acc[i][j]);
   };
-  // mma(f) with the loads of unit kt into buffer buf between its MFMAs (NLA / (I J)
+  // mma(f) with the loads of unit kt into buffer buf between its MFMAs (NL / (I J)
   // after each, same MFMA order as mma): issued together after the barrier, the
   // workgroup's 64 loads of 1 KB queued behind each other while no MFMA was issued.
   auto mma_dma = [&](const Frags& f, int buf, int kt) __attribute__((always_inline)) {
@@ -272,8 +276,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     for (int m = 0; m < NM; ++m) {
       acc[m / J][m % J] = mfma_32x32x16(f.a[m / J], f.b[m % J], acc[m / J][m % J]);
 #pragma unroll
-      for (int i = m * NLA / NM; i < (m + 1) * NLA / NM; ++i)
-        if (!dma_idle && (i < SH::NLB || a_wave)) dma16(rs, dst + i * 1024, vo[i], kt * (kBK * 2));
+      for (int i = m * NL / NM; i < (m + 1) * NL / NM; ++i)
+        if (!dma_idle && has_load(i)) dma16(rs, dst + i * 1024, vo[i], kt * (kBK * 2));
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -288,7 +292,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   constexpr int NT = I * J, CT = 2, NCH = NT / CT;
   const int col = lane & 31, half = lane >> 5;
   auto epilogue_part = [&](int mt, int nt, int h, const f32x16 (&v)[CT]) __attribute__((always_inline)) {
-    const int m0 = mt * kTM + wm * SH::WM + half * 4;
+    const int m0 = mt * TM + wm * SH::WM + half * 4;
     if constexpr (EPI == kSwiGLU) {
       const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(g.act, 0, g.M * g.ffn * 2, kBufWord3);
       const int n = nt * (TN / 2) + wn * 32 + col;
@@ -386,7 +390,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   auto finish = [&](const Cursor& c) __attribute__((always_inline)) {
     int mt, nt;
     tile_mn(c.tile, mt, nt);
-    if (TN == 128 && mt * kTM + wm * SH::WM >= g.M) return;   // every row of this part is past M: nothing to write
+    if (TN == 128 && mt * TM + wm * SH::WM >= g.M) return;    // every row of this part is past M: nothing to write
     if (c.kbeg == 0 && c.kend == p.ks) {
 #pragma unroll
       for (int h = 0; h < NCH; ++h) {
@@ -532,7 +536,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
 #pragma unroll
   for (int b = 0; b < NS; ++b) dma_next(b);
   if (a_wave) wait_vmem<(NS - 1) * NLA>();      // unit 0 of this wavefront
-  else wait_vmem<(NS - 1) * SH::NLB>();
+  else wait_vmem<(NS - 1) * NLB>();
   barrier_lds();                                    // ... of every wavefront
   Frags f0, f1;
   read(f0, 0, 0);
@@ -544,7 +548,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     if constexpr (TN != 128) return true;
     int mt, nt;
     tile_mn(tile, mt, nt);
-    return __builtin_amdgcn_readfirstlane(int(mt * kTM + wm * SH::WM < g.M)) != 0;
+    return __builtin_amdgcn_readfirstlane(int(mt * TM + wm * SH::WM < g.M)) != 0;
   };
   bool live = live_in(cc.tile);
   int u = 0, buf = 0;
@@ -561,7 +565,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
         mma(f0);
       }
       if (a_wave) wait_vmem<(NS - 2) * NLA>();  // this wavefront's loads of unit u + 1
-      else wait_vmem<(NS - 2) * SH::NLB>();
+      else wait_vmem<(NS - 2) * NLB>();
       barrier_lds();
       if (live) {
         read(f0, nbuf, 0);
@@ -601,12 +605,12 @@ int finish_polls() {
   return int(std::min<long>(std::max<long>(v, 0), 1 << 20));
 }
 
-template <int EPI, int TN>
+template <int EPI, int TM, int TN>
 void launch_tn(const GemmArgs& g, bool whole_tiles, hipStream_t stream) {
   static_assert(TN == 128 || TN == 256, "tile width");
   if (TN == 256) whole_tiles = true;                 // the 256-wide kernels finish whole tiles only
   GemmPlan p{};
-  p.m_tiles = cdiv(g.M, kTM);
+  p.m_tiles = cdiv(g.M, TM);
   p.n_tiles = EPI == kSwiGLU ? g.ffn / (TN / 2) : cdiv(g.N, TN);
   p.ks = g.K / kBK;
   p.gm = p.m_tiles < 8 ? p.m_tiles : 8;
@@ -627,18 +631,28 @@ void launch_tn(const GemmArgs& g, bool whole_tiles, hipStream_t stream) {
     p.sk_units = int((tiles - p.dp_tiles) * p.ks);
   }
   p.polls = finish_polls();
-  gemm_kernel<EPI, TN><<<dim3(p.G), kThreads, 0, stream>>>(g, p);
+  gemm_kernel<EPI, TM, TN><<<dim3(p.G), kThreads, 0, stream>>>(g, p);
 }
 
 template <int EPI>
 void launch_epi(const GemmArgs& g, hipStream_t stream) {
   // At least a round of 256 x 256 tiles: whole tiles only (measured: cutting tiles
   // along K costs about one tile time in partial traffic, more than a short last
-  // round).  Fewer: 256 x 128 tiles, cut along K so that every CU gets a share.
+  // round).  The tiles are 256 or 192 rows high, whichever takes less time: a round
+  // of 192-row tiles takes about 15/16 of the time of one of 256-row tiles
+  // (measured; a stage streams the same 256 weight rows), so 192 rows win where
+  // they save a round or more of the short last round: at 736 rows, 448 tiles of
+  // 192 rows in 2 rounds of 224 workgroups instead of 336 of 256 rows in 2 rounds
+  // of 168.  Fewer: 256 x 128 tiles, cut along K so that every CU gets a share.
   const int m_tiles = cdiv(g.M, kTM);
   const int n256 = EPI == kSwiGLU ? (g.ffn % 128 == 0 ? g.ffn / 128 : 0) : cdiv(g.N, 256);
-  if (int64_t(m_tiles) * n256 >= kMaxWorkers) return launch_tn<EPI, 256>(g, true, stream);
-  launch_tn<EPI, 128>(g, false, stream);
+  if (int64_t(m_tiles) * n256 >= kMaxWorkers) {
+    const int64_t r256 = (int64_t(m_tiles) * n256 + kMaxWorkers - 1) / kMaxWorkers;
+    const int64_t r192 = (int64_t(cdiv(g.M, 192)) * n256 + kMaxWorkers - 1) / kMaxWorkers;
+    if (r192 * 15 < r256 * 16) return launch_tn<EPI, 192, 256>(g, true, stream);
+    return launch_tn<EPI, 256, 256>(g, true, stream);
+  }
+  launch_tn<EPI, 256, 128>(g, false, stream);
 }
 
 }  // namespace

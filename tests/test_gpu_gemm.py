@@ -1,8 +1,9 @@
 """GPU parity of the projection GEMM (epic_gemm) against the oracle's plain
 definitions (oracle.projection, float64 on the bf16 operands).
 
-Cases: the four projections of the 32-layer link step (736 rows: 256 x 256 and
-256 x 128 tiles cut along K across workgroups), the same projections at a
+Cases: the four projections of the 32-layer link step (736 rows: 192 x 256 tiles and
+256 x 128 tiles cut along K across workgroups), whole 192-row tiles with row and
+column tails, the same projections at a
 compile-sized row count (whole-tile rounds plus cut tiles; checked on sampled
 rows), row and column tails, tiny shapes, tiles cut into up to 56 parts, the
 fallback finish of cut tiles (bit-identical to the polled one), and m = 0.  Bars: fp32 outputs
@@ -94,6 +95,17 @@ def test_large_row_counts_sampled(m, n, k, epi):
     rng = np.random.default_rng(7)
     sample = sorted(set([0, 1, 255, 256, 257, m - 257, m - 256, m - 1] + rng.integers(0, m, 56).tolist()))
     _run(m, n, k, epi, tag=10 + BIG.index((m, n, k, epi)), sample=sample)
+
+
+TALL = [  # whole tiles of 192 x 256 (fewer rounds x rows than 256 x 256): row and column tails
+    (550, 32768, 256, "store"),         # 3 x 128 tiles in 2 rounds of 192; last row tile 166 rows
+    (600, 24448, 512, "residual"),      # 4 x 96 tiles, last row tile 24 rows, last tile 128 columns
+]
+
+
+@pytest.mark.parametrize("m,n,k,epi", TALL, ids=[f"{c[3]}_{c[0]}x{c[1]}x{c[2]}" for c in TALL])
+def test_192_row_tiles(m, n, k, epi):
+    _run(m, n, k, epi, tag=60 + TALL.index((m, n, k, epi)))
 
 
 SMALL = [
