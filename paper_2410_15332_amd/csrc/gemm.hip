@@ -9,9 +9,9 @@
 //   kRope     : the fused Q|K|V projection: q and k heads rotated at each row's linked
 //               position (rotary pairs (i, i + D/2)), v heads as they are; bf16 q, k, v
 //
-// Tiling: workgroup tile TM x TN (256 x 256, 192 x 256 or 256 x 128), 8 wavefronts of
-// 64 columns each (TN = 256: 2 x 4 wavefronts of TM/2 x 64, i.e. 4 x 2 or 3 x 2
-// v_mfma_f32_32x32x16_bf16 tiles; TN = 128: 4 x 2 wavefronts of 64 x 64).  K runs
+// Tiling: workgroup tile TM x TN (256 x 256, 192 x 256, 256 x 128 or 128 x 128), 8
+// wavefronts of 64 columns each (TN = 256: 2 x 4 wavefronts of TM/2 x 64, i.e. 4 x 2
+// or 3 x 2 v_mfma_f32_32x32x16_bf16 tiles; TN = 128: 4 x 2 wavefronts of TM/4 x 64).  K runs
 // in stages of 64 staged in LDS by direct buffer->LDS loads, NS stages in LDS (2 at
 // TN = 256, 3 at TN = 128; loads issued NS - 1 stages ahead of use).  An operand stage is groups of 8 rows of 128 bytes
 // (one whole cache line per row: a load instruction that covers 16 half lines moves
@@ -29,8 +29,10 @@
 //
 // Scheduling: at most one workgroup per CU (G of them), persistent.  With at least
 // a round of 256 x 256 tiles, whole 256-wide tiles (256 or 192 rows) are dealt in
-// rounds of G, G chosen so the rounds are (nearly) full; 256-wide tiles are never cut.  With fewer tiles (short
-// row sets), 256 x 128 tiles are used and the ones that do not fill whole rounds
+// rounds of G, G chosen so the rounds are (nearly) full; 256-wide tiles are never
+// cut.  With fewer tiles (short row sets): whole 128 x 128 tiles in one round where
+// they fill at least 3/4 of the CUs and K is short; else 256 x 128 tiles, and the
+// ones that do not fill whole rounds
 // (the last partial round plus one full round, or all of them) are cut along K into
 // G equal shares of K stages, one per workgroup, so every CU gets the same work.  A
 // share runs its last segment (the one that starts a tile) first.
@@ -66,7 +68,8 @@ constexpr int kMinUnits = 4;                            // K stages per workgrou
 
 template <int TM, int TN>
 struct Shape {
-  static_assert((TM == 256 && (TN == 128 || TN == 256)) || (TM == 192 && TN == 256), "tile shape");
+  static_assert((TM == 256 && (TN == 128 || TN == 256)) || (TM == 192 && TN == 256) || (TM == 128 && TN == 128),
+                "tile shape");
   static constexpr int NS = TN == 256 ? 2 : 3;          // LDS stages (128 / 112 / 144 KB)
   static constexpr int WAVES_M = TN == 256 ? 2 : 4;     // wavefronts along M
   static constexpr int WM = TM / WAVES_M;               // rows per wavefront
@@ -186,7 +189,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   const bool a_wave = wv < 4;
   // With M <= 128 (one row tile) the A row groups 16..31 hold no row of A: their
   // loading wavefronts issue nothing (none of their waits then has anything to wait for).
-  const bool dma_idle = TN == 128 && a_wave && g.M <= 128 && wv >= 2;
+  const bool dma_idle = TM == 256 && TN == 128 && a_wave && g.M <= 128 && wv >= 2;
   const int nl = a_wave ? NLA : NLB;                   // loads per stage of this wavefront
   const int grp0 = nl * (wv & 3);
   const int lrow = lane >> 3;                              // row within an 8-row group
@@ -643,7 +646,7 @@ void launch_epi(const GemmArgs& g, hipStream_t stream) {
   // (measured; a stage streams the same 256 weight rows), so 192 rows win where
   // they save a round or more of the short last round: at 736 rows, 448 tiles of
   // 192 rows in 2 rounds of 224 workgroups instead of 336 of 256 rows in 2 rounds
-  // of 168.  Fewer: 256 x 128 tiles, cut along K so that every CU gets a share.
+  // of 168.
   const int m_tiles = cdiv(g.M, kTM);
   const int n256 = EPI == kSwiGLU ? (g.ffn % 128 == 0 ? g.ffn / 128 : 0) : cdiv(g.N, 256);
   if (int64_t(m_tiles) * n256 >= kMaxWorkers) {
@@ -652,6 +655,15 @@ void launch_epi(const GemmArgs& g, hipStream_t stream) {
     if (r192 * 15 < r256 * 16) return launch_tn<EPI, 192, 256>(g, true, stream);
     return launch_tn<EPI, 256, 256>(g, true, stream);
   }
+  // Fewer: with one round of 128 x 128 tiles that fills at least 3/4 of the CUs and a
+  // short K, whole 128 x 128 tiles; else 256 x 128 tiles cut along K so that every CU
+  // gets a share.  Measured at 736 rows, N = 4096: whole 128 x 128 tiles take about
+  // 0.57 us per K stage on 192 CUs, the cut tiles about 0.45 us per stage of a tile's K
+  // plus about 15 us of partial traffic and fixup, so whole tiles win up to about 100
+  // stages (W_O, K = 4096: 48.0 -> 40.2 us; W_down, K = 14336: 103.8 -> 127.7 us).
+  const int64_t t128 = int64_t(cdiv(g.M, 128)) * (EPI == kSwiGLU ? g.ffn / 64 : cdiv(g.N, 128));
+  if (t128 >= 3 * kMaxWorkers / 4 && t128 <= kMaxWorkers && g.K / kBK <= 96)
+    return launch_tn<EPI, 128, 128>(g, true, stream);
   launch_tn<EPI, 256, 128>(g, false, stream);
 }
 

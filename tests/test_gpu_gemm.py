@@ -1,9 +1,9 @@
 """GPU parity of the projection GEMM (epic_gemm) against the oracle's plain
 definitions (oracle.projection, float64 on the bf16 operands).
 
-Cases: the four projections of the 32-layer link step (736 rows: 192 x 256 tiles and
-256 x 128 tiles cut along K across workgroups), whole 192-row tiles with row and
-column tails, the same projections at a
+Cases: the four projections of the 32-layer link step (736 rows: whole 192 x 256 and
+128 x 128 tiles, 256 x 128 tiles cut along K across workgroups), whole 192-row tiles with row
+and column tails, whole 128-row tiles with row tails, the same projections at a
 compile-sized row count (whole-tile rounds plus cut tiles; checked on sampled
 rows), row and column tails, tiny shapes, tiles cut into up to 56 parts, the
 fallback finish of cut tiles (bit-identical to the polled one), and m = 0.  Bars: fp32 outputs
@@ -108,6 +108,17 @@ def test_192_row_tiles(m, n, k, epi):
     _run(m, n, k, epi, tag=60 + TALL.index((m, n, k, epi)))
 
 
+WHOLE128 = [  # one round of whole 128 x 128 tiles (short K, >= 192 tiles): row tails (n % 128 == 0)
+    (760, 4096, 2048, "store"),         # 6 x 32 tiles, last row tile 120 rows
+    (700, 4096, 1024, "swiglu"),        # ffn 2048: 6 x 32 tiles of 64 outputs, last row tile 60 rows
+]
+
+
+@pytest.mark.parametrize("m,n,k,epi", WHOLE128, ids=[f"{c[3]}_{c[0]}x{c[1]}x{c[2]}" for c in WHOLE128])
+def test_whole_128_tiles(m, n, k, epi):
+    _run(m, n, k, epi, tag=70 + WHOLE128.index((m, n, k, epi)))
+
+
 SMALL = [
     (1, 128, 64, "store"),
     (28, 384, 256, "residual"),
@@ -155,7 +166,7 @@ def test_cut_tile_fallback_matches_fast_path(m, n, k, epi, monkeypatch):
 def test_repeated_calls_reuse_workspace():
     """Back-to-back calls on one workspace: the split-tile counters are reset."""
     for _ in range(2):
-        _run(736, 4096, 4096, "residual", tag=30)
+        _run(736, 6144, 4096, "residual", tag=30)     # 256 x 128 tiles cut along K
         _run(300, 1024, 512, "store", tag=31)
 
 
