@@ -36,21 +36,28 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __re
                                                                uint16_t* __restrict__ out_bf16,
                                                                float* __restrict__ out_f32, int hidden, float eps) {
   // The row stays in registers between the two passes (up to kKeep float4 per
-  // thread, hidden <= 8192 at 256 threads); a longer row is read again.
+  // thread, hidden <= 8192 at 256 threads); a longer row is read again.  The kept
+  // part's loads, and its weights, are issued together from clamped indices (no
+  // branch between them, so one wait covers them all); slots past the row add an
+  // exact 0 to the sum of squares, which leaves it as the in-order sum of the row.
   constexpr int kKeep = 8;
   __shared__ float red[kNormThreads / 64];
   const int row = blockIdx.x;
   const float4* xr = reinterpret_cast<const float4*>(x + size_t(row) * hidden);
   const int n4 = hidden / 4;
   float4 keep[kKeep];
+  uint2 keep_w[kKeep];
+#pragma unroll
+  for (int k = 0; k < kKeep; ++k) {
+    const int i = min(int(threadIdx.x) + k * kNormThreads, n4 - 1);
+    keep[k] = xr[i];
+    keep_w[k] = *reinterpret_cast<const uint2*>(w + 4 * i);
+  }
   float ss = 0.0f;
 #pragma unroll
   for (int k = 0; k < kKeep; ++k) {
-    const int i = threadIdx.x + k * kNormThreads;
-    if (i < n4) {
-      keep[k] = xr[i];
-      ss += keep[k].x * keep[k].x + keep[k].y * keep[k].y + keep[k].z * keep[k].z + keep[k].w * keep[k].w;
-    }
+    const float sq = keep[k].x * keep[k].x + keep[k].y * keep[k].y + keep[k].z * keep[k].z + keep[k].w * keep[k].w;
+    ss += int(threadIdx.x) + k * kNormThreads < n4 ? sq : 0.0f;
   }
   for (int i = threadIdx.x + kKeep * kNormThreads; i < n4; i += kNormThreads) {
     const float4 v = xr[i];
@@ -58,8 +65,7 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __re
   }
   const float total = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(total / float(hidden) + eps);
-  auto put = [&](int i, const float4& v) {
-    const uint2 wb = *reinterpret_cast<const uint2*>(w + 4 * i);
+  auto put = [&](int i, const float4& v, const uint2& wb) {
     const float y0 = v.x * inv * bf16_to_f32(uint16_t(wb.x & 0xFFFFu));
     const float y1 = v.y * inv * bf16_to_f32(uint16_t(wb.x >> 16));
     const float y2 = v.z * inv * bf16_to_f32(uint16_t(wb.y & 0xFFFFu));
@@ -74,9 +80,10 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const float* __re
 #pragma unroll
   for (int k = 0; k < kKeep; ++k) {
     const int i = threadIdx.x + k * kNormThreads;
-    if (i < n4) put(i, keep[k]);
+    if (i < n4) put(i, keep[k], keep_w[k]);
   }
-  for (int i = threadIdx.x + kKeep * kNormThreads; i < n4; i += kNormThreads) put(i, xr[i]);
+  for (int i = threadIdx.x + kKeep * kNormThreads; i < n4; i += kNormThreads)
+    put(i, xr[i], *reinterpret_cast<const uint2*>(w + 4 * i));
 }
 
 // cs[row][i] = (cos, sin)(s_pos[row] * theta^(-2i/D)), float64 angle.
