@@ -693,8 +693,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the link step is built and timed on a single MI355X; "
-              "the link step runs on one GPU; sharding across GPUs is not built. Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU: the link step is built and timed on a single MI355X, and "
+              "sharding across GPUs is not built. Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
