@@ -68,10 +68,13 @@ constexpr int kMinUnits = 4;                            // K stages per workgrou
 
 template <int TM, int TN>
 struct Shape {
-  static_assert((TM == 256 && (TN == 128 || TN == 256)) || (TM == 192 && TN == 256) || (TM == 128 && TN == 128),
+  static_assert((TM == 256 && (TN == 128 || TN == 256)) || (TM == 192 && TN == 256) ||
+                    ((TM == 128 || TM == 96) && TN == 128),
                 "tile shape");
-  static constexpr int NS = TN == 256 ? 2 : 3;          // LDS stages (128 / 112 / 144 KB)
-  static constexpr int WAVES_M = TN == 256 ? 2 : 4;     // wavefronts along M
+  static constexpr int NS = TN == 256 ? 2 : 3;          // LDS stages (128 / 112 / 144 / 96 / 84 KB)
+  // wavefronts along M (TM = 96: 3 x 2 wavefronts compute, the other two only stage
+  // operands and meet the barriers)
+  static constexpr int WAVES_M = TN == 256 ? 2 : TM >= 128 ? 4 : TM / 32;
   static constexpr int WM = TM / WAVES_M;               // rows per wavefront
   static constexpr int I = WM / 32;                     // 32-row MFMA tiles per wavefront
   static constexpr int J = 2;                           // 32-column MFMA tiles per wavefront
@@ -135,7 +138,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   // wavefront tile: rows wm*WM.., columns wn*64..  At TN = 128 the two wavefronts of
   // each SIMD (wavefronts w and w + 4) take different row halves, so a tile whose
-  // rows past M leave half the wavefronts idle still keeps every SIMD busy.
+  // rows past M leave half the wavefronts idle still keeps every SIMD busy.  Wavefronts
+  // with wm >= WAVES_M (TM = 96: wavefronts 6 and 7) compute and store nothing.
   const int wm = TN == 128 ? wv >> 1 : wv % SH::WAVES_M;
   const int wn = TN == 128 ? wv & 1 : wv / SH::WAVES_M;
   const int w = blockIdx.x;
@@ -393,7 +397,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
   auto finish = [&](const Cursor& c) __attribute__((always_inline)) {
     int mt, nt;
     tile_mn(c.tile, mt, nt);
-    if (TN == 128 && mt * TM + wm * SH::WM >= g.M) return;    // every row of this part is past M: nothing to write
+    // no rows of this part (past the tile, or every row past M): nothing to write
+    if (TN == 128 && (wm >= SH::WAVES_M || mt * TM + wm * SH::WM >= g.M)) return;
     if (c.kbeg == 0 && c.kend == p.ks) {
 #pragma unroll
       for (int h = 0; h < NCH; ++h) {
@@ -551,7 +556,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g, GemmPlan 
     if constexpr (TN != 128) return true;
     int mt, nt;
     tile_mn(tile, mt, nt);
-    return __builtin_amdgcn_readfirstlane(int(mt * TM + wm * SH::WM < g.M)) != 0;
+    return __builtin_amdgcn_readfirstlane(int(wm < SH::WAVES_M && mt * TM + wm * SH::WM < g.M)) != 0;
   };
   bool live = live_in(cc.tile);
   int u = 0, buf = 0;
@@ -661,9 +666,16 @@ void launch_epi(const GemmArgs& g, hipStream_t stream) {
   // 0.57 us per K stage on 192 CUs, the cut tiles about 0.45 us per stage of a tile's K
   // plus about 15 us of partial traffic and fixup, so whole tiles win up to about 100
   // stages (W_O, K = 4096: 48.0 -> 40.2 us; W_down, K = 14336: 103.8 -> 127.7 us).
-  const int64_t t128 = int64_t(cdiv(g.M, 128)) * (EPI == kSwiGLU ? g.ffn / 64 : cdiv(g.N, 128));
-  if (t128 >= 3 * kMaxWorkers / 4 && t128 <= kMaxWorkers && g.K / kBK <= 96)
-    return launch_tn<EPI, 128, 128>(g, true, stream);
+  const int64_t n128 = EPI == kSwiGLU ? g.ffn / 64 : cdiv(g.N, 128);
+  const int64_t t128 = int64_t(cdiv(g.M, 128)) * n128, t96 = int64_t(cdiv(g.M, 96)) * n128;
+  auto one_round = [](int64_t t) { return t >= 3 * kMaxWorkers / 4 && t <= kMaxWorkers; };
+  if (g.K / kBK <= 96) {
+    // 96 rows where they make one round of more workgroups: a stage's time goes with
+    // the bytes a CU stages, not with the number of CUs (W_O at 736 rows: 256 tiles of
+    // 96 x 128 against 192 of 128 x 128)
+    if (one_round(t96)) return launch_tn<EPI, 96, 128>(g, true, stream);
+    if (one_round(t128)) return launch_tn<EPI, 128, 128>(g, true, stream);
+  }
   launch_tn<EPI, 256, 128>(g, false, stream);
 }
 

@@ -2,8 +2,8 @@
 definitions (oracle.projection, float64 on the bf16 operands).
 
 Cases: the four projections of the 32-layer link step (736 rows: whole 192 x 256 and
-128 x 128 tiles, 256 x 128 tiles cut along K across workgroups), whole 192-row tiles with row
-and column tails, whole 128-row tiles with row tails, the same projections at a
+96 x 128 tiles, 256 x 128 tiles cut along K across workgroups), whole 192-row tiles with row
+and column tails, whole 96- and 128-row tiles with row tails, the same projections at a
 compile-sized row count (whole-tile rounds plus cut tiles; checked on sampled
 rows), row and column tails, tiny shapes, tiles cut into up to 56 parts, the
 fallback finish of cut tiles (bit-identical to the polled one), and m = 0.  Bars: fp32 outputs
@@ -108,15 +108,17 @@ def test_192_row_tiles(m, n, k, epi):
     _run(m, n, k, epi, tag=60 + TALL.index((m, n, k, epi)))
 
 
-WHOLE128 = [  # one round of whole 128 x 128 tiles (short K, >= 192 tiles): row tails (n % 128 == 0)
-    (760, 4096, 2048, "store"),         # 6 x 32 tiles, last row tile 120 rows
-    (700, 4096, 1024, "swiglu"),        # ffn 2048: 6 x 32 tiles of 64 outputs, last row tile 60 rows
+WHOLE_NARROW = [  # one round of whole 96 x 128 or 128 x 128 tiles (short K): row tails (n % 128 == 0)
+    (760, 4096, 2048, "store"),         # 8 x 32 tiles of 96 rows, last row tile 88 rows
+    (700, 4096, 1024, "swiglu"),        # ffn 2048: 8 x 32 tiles of 96 x 64 outputs, last row tile 28 rows
+    (800, 4096, 2048, "store"),         # 9 x 32 tiles of 96 rows would be 288: 7 x 32 of 128, last 32 rows
+    (200, 14336, 1024, "swiglu"),       # ffn 7168: 2 x 112 tiles of 128 x 64 outputs, last row tile 72 rows
 ]
 
 
-@pytest.mark.parametrize("m,n,k,epi", WHOLE128, ids=[f"{c[3]}_{c[0]}x{c[1]}x{c[2]}" for c in WHOLE128])
-def test_whole_128_tiles(m, n, k, epi):
-    _run(m, n, k, epi, tag=70 + WHOLE128.index((m, n, k, epi)))
+@pytest.mark.parametrize("m,n,k,epi", WHOLE_NARROW, ids=[f"{c[3]}_{c[0]}x{c[1]}x{c[2]}" for c in WHOLE_NARROW])
+def test_whole_narrow_tiles(m, n, k, epi):
+    _run(m, n, k, epi, tag=70 + WHOLE_NARROW.index((m, n, k, epi)))
 
 
 SMALL = [
