@@ -45,7 +45,7 @@ extern "C" {
 typedef enum {
   EPIC_OK = 0,
   EPIC_ERR_INVALID_ARG = 1,     /* malformed sizes, ids out of range, NULL where data is needed */
-  EPIC_ERR_UNSUPPORTED = 2,     /* a shape this build does not implement */
+  EPIC_ERR_UNSUPPORTED = 2,     /* a shape the library does not implement */
   EPIC_ERR_NO_PRIVATE_BLOCKS = 3,/* free list shorter than the plan needs */
   EPIC_ERR_WORKSPACE = 4,       /* workspace smaller than required */
   EPIC_ERR_HIP = 5              /* a HIP runtime call failed (launch error) */

@@ -1,5 +1,5 @@
 """bench.py's command-line contract on the CPU: more than one GPU is refused with a
-message (this build measures one GPU), and every workload name it offers is one the
+message (bench.py measures one GPU), and every workload name it offers is one the
 configuration table knows."""
 import os
 import subprocess
