@@ -660,19 +660,18 @@ void launch_epi(const GemmArgs& g, hipStream_t stream) {
     if (r192 * 15 < r256 * 16) return launch_tn<EPI, 192, 256>(g, true, stream);
     return launch_tn<EPI, 256, 256>(g, true, stream);
   }
-  // Fewer: with one round of 128 x 128 tiles that fills at least 3/4 of the CUs and a
-  // short K, whole 128 x 128 tiles; else 256 x 128 tiles cut along K so that every CU
-  // gets a share.  Measured at 736 rows, N = 4096: whole 128 x 128 tiles take about
-  // 0.57 us per K stage on 192 CUs, the cut tiles about 0.45 us per stage of a tile's K
-  // plus about 15 us of partial traffic and fixup, so whole tiles win up to about 100
-  // stages (W_O, K = 4096: 48.0 -> 40.2 us; W_down, K = 14336: 103.8 -> 127.7 us).
+  // Fewer: with a short K and one round of 96 x 128 or 128 x 128 tiles that fills at
+  // least 3/4 of the CUs, those tiles whole (96 rows where they make such a round: more
+  // CUs, fewer bytes each); else 256 x 128 tiles cut along K so that every CU gets a
+  // share.  Measured at 736 rows, N = 4096: whole 128 x 128 tiles take about 0.57 us per
+  // K stage on 192 CUs, the cut tiles about 0.45 us per stage of a tile's K plus about
+  // 15 us of partial traffic and fixup, so whole tiles win up to about 100 stages (W_O,
+  // K = 4096: 48.0 -> 40.2 us; W_down, K = 14336: 103.8 -> 127.7 us).  96 x 128 tiles on
+  // 256 CUs took W_O about 1 us further (the c3 link step 0.3% faster on one box).
   const int64_t n128 = EPI == kSwiGLU ? g.ffn / 64 : cdiv(g.N, 128);
   const int64_t t128 = int64_t(cdiv(g.M, 128)) * n128, t96 = int64_t(cdiv(g.M, 96)) * n128;
   auto one_round = [](int64_t t) { return t >= 3 * kMaxWorkers / 4 && t <= kMaxWorkers; };
   if (g.K / kBK <= 96) {
-    // 96 rows where they make one round of more workgroups: a stage's time goes with
-    // the bytes a CU stages, not with the number of CUs (W_O at 736 rows: 256 tiles of
-    // 96 x 128 against 192 of 128 x 128)
     if (one_round(t96)) return launch_tn<EPI, 96, 128>(g, true, stream);
     if (one_round(t128)) return launch_tn<EPI, 128, 128>(g, true, stream);
   }
