@@ -9,11 +9,13 @@
 //   kRope     : the fused Q|K|V projection: q and k heads rotated at each row's linked
 //               position (rotary pairs (i, i + D/2)), v heads as they are; bf16 q, k, v
 //
-// Tiling: workgroup tile TM x TN (256 x 256, 192 x 256, 256 x 128 or 128 x 128), 8
-// wavefronts of 64 columns each (TN = 256: 2 x 4 wavefronts of TM/2 x 64, i.e. 4 x 2
-// or 3 x 2 v_mfma_f32_32x32x16_bf16 tiles; TN = 128: 4 x 2 wavefronts of TM/4 x 64).  K runs
-// in stages of 64 staged in LDS by direct buffer->LDS loads, NS stages in LDS (2 at
-// TN = 256, 3 at TN = 128; loads issued NS - 1 stages ahead of use).  An operand stage is groups of 8 rows of 128 bytes
+// Tiling: workgroup tile TM x TN (256 x 256, 192 x 256, 256 x 128, 128 x 128 or
+// 96 x 128), 8 wavefronts of 64 columns each (TN = 256: 2 x 4 wavefronts of TM/2 x 64,
+// i.e. 4 x 2 or 3 x 2 v_mfma_f32_32x32x16_bf16 tiles; TN = 128: 4 x 2 wavefronts of
+// TM/4 x 64, and at TM = 96 3 x 2 of 32 x 64 while the other two only stage
+// operands).  K runs in stages of 64 staged in LDS by direct buffer->LDS loads, NS
+// stages in LDS (2 at TN = 256, 3 at TN = 128; loads issued NS - 1 stages ahead of
+// use).  An operand stage is groups of 8 rows of 128 bytes
 // (one whole cache line per row: a load instruction that covers 16 half lines moves
 // about 0.6x the bytes per cycle of one that covers 8 whole lines); row r sits at byte
 // 128 r with its eight 16-byte chunks XOR-swizzled by (r / 2) % 8, so one load
@@ -30,9 +32,9 @@
 // Scheduling: at most one workgroup per CU (G of them), persistent.  With at least
 // a round of 256 x 256 tiles, whole 256-wide tiles (256 or 192 rows) are dealt in
 // rounds of G, G chosen so the rounds are (nearly) full; 256-wide tiles are never
-// cut.  With fewer tiles (short row sets): whole 128 x 128 tiles in one round where
-// they fill at least 3/4 of the CUs and K is short; else 256 x 128 tiles, and the
-// ones that do not fill whole rounds
+// cut.  With fewer tiles (short row sets): whole 96 x 128 or 128 x 128 tiles in one
+// round where they fill at least 3/4 of the CUs and K is short; else 256 x 128 tiles,
+// and the ones that do not fill whole rounds
 // (the last partial round plus one full round, or all of them) are cut along K into
 // G equal shares of K stages, one per workgroup, so every CU gets the same work.  A
 // share runs its last segment (the one that starts a tile) first.
